@@ -1,0 +1,428 @@
+"""Pins of the CPU oracle against the paper and the mathematics (CPU only).
+
+Each test checks the oracle against something that is not the oracle: a
+brute-force scan or LP (oracle/brute.py), a closed form the paper states, an
+invariance of the definition, or a textbook routine.  The pins are chosen so
+that a dropped term, a wrong sign or index, or a transposed operand in
+dro_oracle.c fails at least one of them.
+"""
+import math
+from fractions import Fraction as F
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import brute
+from workloads import make_workload, random_workload, lam_grid, eta_grid
+from workloads.configs import Workload
+
+
+def _tiny(seed, C=2, N=(6, 9), L=40, K=9, M=7, E=3, **kw):
+    return random_workload(seed=seed, C=C, N=N, L=L, K=K, M=M, E=E, **kw)
+
+
+# ---------------------------------------------------------------- P1 -------
+# Step 4 of Appendix A: the supremum over [0, L] sits at 0, at the sample or
+# at L.  The closed form must equal an exhaustive scan of the support.
+
+@pytest.mark.parametrize("seed", range(6))
+def test_P1_phi_closed_form_equals_scanned_supremum(seed):
+    rng = np.random.default_rng(100 + seed)
+    L = int(rng.integers(1, 64))
+    for _ in range(60):
+        eta = int(rng.integers(0, L + 1))
+        x = int(rng.integers(0, L + 1))
+        cp = float(np.float32(rng.choice([0.5, 1, 2, 3.25, 8, 17.5, 64.0])))
+        cw = float(np.float32(rng.choice([0.25, 0.5, 1, 1.5, 4.0])))
+        lam = float(np.float32(rng.choice([0.001, 0.3, 1.0, 2.5, 7.75, 33.0, 100.0])))
+        want = brute.sup_brute(eta, x, L, cp, cw, lam, steps=2 * L)
+        got_fix = oracle.phi_fix(eta, x, L, cp, cw, lam)
+        assert F(got_fix, 1 << 33) == want, (eta, x, L, cp, cw, lam)
+        got64 = oracle.phi(eta, x, L, cp, cw, lam)
+        assert abs(got64 - float(want)) <= 1e-12 * max(1.0, abs(float(want)))
+
+
+def test_P1_edges():
+    # eta at 0 and at L, samples at 0 and at L, and a multiplier above and below both costs
+    L = 10
+    for eta in (0, L):
+        for x in (0, L, 3):
+            for lam in (float(np.float32(v)) for v in (0.001, 1.0, 100.0)):
+                want = brute.sup_brute(eta, x, L, 4.0, 1.0, lam, steps=40)
+                assert F(oracle.phi_fix(eta, x, L, 4.0, 1.0, lam), 1 << 33) == want
+
+
+# ---------------------------------------------------------------- P2 -------
+# Strong duality (eq. app_strong_duality) and the LP of Step 5: the
+# transport-plan primal equals the continuous-gamma dual; the grid dual
+# (what the path computes) is an upper bound, tight when the grid holds the
+# minimising gamma.
+
+@pytest.mark.parametrize("seed", range(5))
+def test_P2_primal_lp_equals_dual(seed):
+    rng = np.random.default_rng(200 + seed)
+    L = int(rng.integers(4, 12))
+    N = int(rng.integers(1, 5))
+    xs = [int(v) for v in rng.integers(0, L + 1, N)]
+    eta = int(rng.integers(0, L + 1))
+    cp = float(rng.choice([1.0, 2.0, 5.0, 8.0]))
+    cw = float(rng.choice([0.5, 1.0, 2.0]))
+    eps = float(rng.choice([0.0, 0.25, 1.0, 2.5]))
+    lp = brute.worst_case_lp(eta, xs, L, cp, cw, eps)
+    dv, _ = brute.dual_exact(eta, xs, L, cp, cw, eps)
+    assert abs(lp - float(dv)) <= 1e-9 * max(1.0, abs(lp))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_P2_grid_dual_upper_bound_and_tight_on_breakpoint(seed):
+    rng = np.random.default_rng(300 + seed)
+    L, N = 24, 5
+    xs = np.sort(rng.integers(0, L + 1, N)).astype(np.int32)
+    cp, cw = np.float32(rng.choice([2.0, 4.0, 8.0])), np.float32(rng.choice([0.5, 1.0]))
+    eps = np.float32(rng.choice([0.5, 2.0, 6.0]))
+    eta = eta_grid(7, L)
+    lam = lam_grid(9)
+    for k in range(eta.size):
+        dv, gstar = brute.dual_exact(int(eta[k]), xs.tolist(), L, float(cp), float(cw), float(eps))
+        # grid that holds the minimiser (a binary32 value whenever gstar is exact in binary32)
+        grids = [lam]
+        if gstar > 0 and F(float(np.float32(float(gstar)))) == gstar:
+            grids.append(np.unique(np.append(lam, np.float32(float(gstar)))).astype(np.float32))
+        for g in grids:
+            w = Workload("t", 1, np.array([0, N], np.int64), None, xs, np.array([L], np.int32),
+                         eta, g, np.array([cp], np.float32), np.array([cw], np.float32), 1,
+                         np.array([eps], np.float32))
+            W, _ = oracle.W_table(w, oracle.S_exact(w, grouped=False))
+            assert W[0, 0, k] >= float(dv) * (1 - 1e-15)
+            if g is not lam:
+                assert abs(W[0, 0, k] - float(dv)) <= 1e-13 * max(1.0, float(dv))
+
+
+# ---------------------------------------------------------------- P3/P4 ----
+# Prop. 4.2 at eps = 0: the worst case is the empirical distribution, so the
+# cost is the SAA cost and the optimal reservation is the empirical quantile
+# at the critical fractile c_p / (c_p + c_w).
+
+@pytest.mark.parametrize("seed", range(4))
+def test_P3_eps0_equals_saa(seed):
+    w = _tiny(seed, E=1)
+    w.eps[:] = 0
+    W, _ = oracle.W_table(w, oracle.S_exact(w))
+    for c in range(w.C):
+        xs = w.samples_of(c).tolist()
+        for k in range(w.K):
+            want = brute.saa_exact(int(w.eta[k]), xs, float(w.c_p[c]), float(w.c_w[c]))
+            # J = RN(RN(S) / N) with S exact: compare against the exact rational
+            assert abs(W[0, c, k] - float(want)) <= 2.3e-16 * float(want) + 1e-300
+
+
+@pytest.mark.parametrize("name", ["cfg1", "cfg2"])
+def test_P4_critical_fractile_brackets_argmin(name):
+    w = make_workload(name)
+    w.eps[:] = 0
+    r = oracle.solve(w)
+    for c in range(w.C):
+        q = int(r["q_value"][c])
+        lo = int(np.searchsorted(w.eta, q, side="right") - 1)   # largest eta <= q
+        hi = int(np.searchsorted(w.eta, q, side="left"))        # smallest eta >= q
+        assert int(r["k_star"][0, c]) in {lo, hi}
+
+
+def test_P4_quantile_minimises_saa_on_random_data():
+    for seed in range(5):
+        w = _tiny(seed, L=60, K=61, E=1)       # grid = every integer: the quantile is a grid point
+        w.eps[:] = 0
+        r = oracle.solve(w)
+        for c in range(w.C):
+            assert w.eta[r["k_star"][0, c]] == r["q_value"][c]
+
+
+# ---------------------------------------------------------------- P5/P6 ----
+# Appendix structure: for gamma >= max(c_p, c_w) every sample keeps its own
+# point, so S equals the SAA sum; when eps <= D(eta) the continuous dual is
+# max(c_p, c_w) eps + SAA.
+
+@pytest.mark.parametrize("seed", range(4))
+def test_P5_large_multiplier_gives_saa_sum(seed):
+    w = _tiny(seed, E=1)
+    S = oracle.S_exact(w)
+    for c in range(w.C):
+        xs = w.samples_of(c).tolist()
+        top = max(float(w.c_p[c]), float(w.c_w[c]))
+        for k in range(w.K):
+            saa_sum = brute.saa_exact(int(w.eta[k]), xs, float(w.c_p[c]), float(w.c_w[c])) * len(xs)
+            for m in range(w.M):
+                if float(w.lam[m]) >= top:
+                    assert F(S.as_int((c, k, m)), 1 << 33) == saa_sum
+
+
+def _D(eta, xs, L, cp, cw):
+    if cp >= cw:
+        return sum((F(L - x) for x in xs if eta <= x < L), F(0)) / len(xs)
+    return sum((F(x) for x in xs if 0 < x <= eta), F(0)) / len(xs)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_P5_small_radius_identity(seed):
+    rng = np.random.default_rng(500 + seed)
+    L = 30
+    xs = [int(v) for v in rng.integers(0, L + 1, 6)]
+    cp, cw = float(rng.choice([2.0, 4.0, 0.5])), float(rng.choice([1.0, 0.25]))
+    for eta in range(0, L + 1, 5):
+        D = _D(eta, xs, L, cp, cw)
+        for eps in (F(0), D / 3, D):
+            dv, _ = brute.dual_exact(eta, xs, L, cp, cw, eps)
+            assert dv == max(F(cp), F(cw)) * eps + brute.saa_exact(eta, xs, cp, cw)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_P6_bounds(seed):
+    w = _tiny(seed)
+    r = oracle.solve(w)
+    W = r["W"]
+    for e in range(w.E):
+        for c in range(w.C):
+            xs = w.samples_of(c).tolist()
+            eps = float(w.eps[e * w.C + c])
+            for k in range(w.K):
+                eta = int(w.eta[k])
+                saa = float(brute.saa_exact(eta, xs, float(w.c_p[c]), float(w.c_w[c])))
+                tol = 1e-12 * max(1.0, saa)
+                assert W[e, c, k] >= saa - tol
+                assert W[e, c, k] <= float(w.lam[-1]) * eps + saa + tol
+                hi2 = float(w.lam[0]) * eps + max(float(w.c_w[c]) * eta,
+                                                  float(w.c_p[c]) * (int(w.L[c]) - eta))
+                assert W[e, c, k] <= hi2 + tol
+
+
+# ---------------------------------------------------------------- P7 -------
+# W is non-decreasing and concave in eps (a min over m of lines in eps with
+# slopes lam_m >= 0); with J = RN(lam*eps) + fixed RN(S/N) the monotonicity
+# holds bit for bit.
+
+def test_P7_monotone_concave_in_radius():
+    w = _tiny(11, E=1, N=(40, 25))
+    S = oracle.S_exact(w)
+    radii = np.linspace(0, 12, 25).astype(np.float32)
+    rows = []
+    for r in radii:
+        Wr, _ = oracle.W_table(w, S, eps=np.full(w.C, r, np.float32), E=1)
+        rows.append(Wr[0])
+    rows = np.array(rows)                       # [R, C, K]
+    assert np.all(np.diff(rows, axis=0) >= 0)
+    second = rows[2:] - 2 * rows[1:-1] + rows[:-2]
+    assert np.all(second <= 1e-9 * np.abs(rows[1:-1]).max())
+
+
+# ---------------------------------------------------------------- P8-P10 ---
+
+def test_P8_power_of_two_scaling_is_exact():
+    w = _tiny(21, lam_lo=0.01)          # keeps lam * 2^-3 inside the exact range
+    base = oracle.solve(w)
+    for s in (-3, 2):
+        f = np.float32(2.0 ** s)
+        w2 = _tiny(21, lam_lo=0.01)
+        w2.c_p = (w.c_p * f).astype(np.float32)
+        w2.c_w = (w.c_w * f).astype(np.float32)
+        w2.lam = (w.lam * f).astype(np.float32)
+        r2 = oracle.solve(w2)
+        assert np.array_equal(r2["W"], base["W"] * float(f))
+        assert np.array_equal(r2["k_star"], base["k_star"])
+        assert np.array_equal(r2["m_star"], base["m_star"])
+        assert np.array_equal(r2["q_value"], base["q_value"])
+
+
+def test_P9_permutation_invariance():
+    w = _tiny(31, N=(30, 17))
+    base = oracle.solve(w)
+    rng = np.random.default_rng(0)
+    w2 = _tiny(31, N=(30, 17))
+    for c in range(w2.C):
+        a, b = w2.offsets[c], w2.offsets[c + 1]
+        w2.xi[a:b] = rng.permutation(w2.xi[a:b])
+    r2 = oracle.solve(w2, grouped=False)
+    for key in ("W", "k_star", "m_star", "W_star", "q_value", "q_rank"):
+        assert np.array_equal(r2[key], base[key]), key
+
+
+def test_P10_segment_reorder_and_alias():
+    w = _tiny(41, C=3, N=(12, 20, 7))
+    base = oracle.solve(w)
+    # reorder segments in memory and alias two extra classes onto existing segments
+    order = [2, 0, 1]
+    parts = [w.samples_of(c) for c in order]
+    off = np.zeros(4, np.int64)
+    off[1:] = np.cumsum([len(p) for p in parts])
+    seg = np.array([order.index(c) for c in range(3)] + [order.index(1), order.index(0)], np.int32)
+    ext = [0, 1, 2, 1, 0]
+    w2 = Workload("alias", 5, off, seg, np.concatenate(parts).astype(np.int32),
+                  np.full(5, w.L[0], np.int32), w.eta, w.lam,
+                  w.c_p[ext].astype(np.float32), w.c_w[ext].astype(np.float32), w.E,
+                  np.concatenate([w.eps[e * 3:(e + 1) * 3][ext] for e in range(w.E)]).astype(np.float32))
+    r2 = oracle.solve(w2)
+    for e in range(w.E):
+        for c2, c in enumerate(ext):
+            assert np.array_equal(r2["W"][e, c2], base["W"][e, c])
+            assert r2["k_star"][e, c2] == base["k_star"][e, c]
+    assert np.array_equal(r2["q_value"], base["q_value"][ext])
+
+
+# ---------------------------------------------------------------- P11 ------
+# Generalized inverse of the empirical CDF: the ceil(qN)-th order statistic.
+
+def test_P11_rank_is_exact():
+    rng = np.random.default_rng(7)
+    for _ in range(400):
+        cp = np.float32(np.exp(rng.uniform(-6, 4.8)))
+        cw = np.float32(np.exp(rng.uniform(-6, 4.8)))
+        N = int(rng.integers(1, 1 << 26))
+        assert oracle.rank(cp, cw, N) == brute.rank_exact(float(cp), float(cw), N)
+    # q N an integer: rho = 4 with N = 100000 gives j = 80000 exactly
+    assert oracle.rank(4.0, 1.0, 100000) == 80000
+    assert oracle.rank(8.0, 1.0, 9) == 8
+
+
+@pytest.mark.parametrize("name", ["cfg1", "cfg2"])
+def test_P11_quantile_matches_partition(name):
+    w = make_workload(name)
+    qv, qr = oracle.quantile(w)
+    for c in range(w.C):
+        x = w.samples_of(c)
+        j = brute.rank_exact(float(w.c_p[c]), float(w.c_w[c]), len(x))
+        assert qr[c] == j
+        assert qv[c] == np.partition(x, j - 1)[j - 1]
+
+
+# ---------------------------------------------------------------- P12 ------
+# Two independent summations: dense fp64 in sample order vs exact integers.
+
+def test_P12_dense_f64_matches_exact():
+    for w in (make_workload("cfg1"), _tiny(51, N=(300, 41), L=900, K=33, M=17)):
+        d = oracle.S_f64(w)
+        x = oracle.S_exact(w).to_double()
+        assert np.max(np.abs(d - x) / np.maximum(x, 1e-300)) <= 1e-12
+
+
+def test_P12_grouped_equals_per_sample():
+    w = _tiny(61, N=(80, 33))
+    a, b = oracle.S_exact(w, grouped=True), oracle.S_exact(w, grouped=False)
+    assert np.array_equal(a.hi, b.hi) and np.array_equal(a.lo, b.lo)
+
+
+def test_fix_to_double_is_correctly_rounded():
+    rng = np.random.default_rng(3)
+    for _ in range(2000):
+        bits = int(rng.integers(1, 82))
+        v = int(rng.integers(0, 1 << 62)) << max(0, bits - 62) | int(rng.integers(0, 1 << 20))
+        v &= (1 << bits) - 1
+        hi, lo = v >> 64, v & ((1 << 64) - 1)
+        want = float(F(v, 1 << 33))        # Python rounds rationals to nearest, ties to even
+        assert oracle._load().oracle_fix_to_double(hi, lo) == want
+    # a tie exactly halfway between two doubles rounds to even
+    v = (1 << 60) + (1 << 7)               # 2^60 + 2^7: halfway at 53-bit precision
+    assert oracle._load().oracle_fix_to_double(v >> 64, v & ((1 << 64) - 1)) == float(F(v, 1 << 33))
+
+
+# ---------------------------------------------------------------- P13 ------
+# The block step: each class takes the exact best grid point that keeps every
+# group it is routed to within capacity (eq. capacity), given the others;
+# the sweep never increases the summed cost from a feasible start.
+
+def _feasible_kmax_exact(w, c, kcur):
+    g = w.groups
+    G = g.G
+    one_k = 1 + F(float(np.float32(g.kappa)))
+    best = None
+    for gg in range(G):
+        u = F(float(g.conc[c * G + gg]))
+        if u <= 0:
+            continue
+        other = one_k * sum((F(float(g.conc[c2 * G + gg])) * int(w.eta[kcur[c2]])
+                             for c2 in range(w.C) if c2 != c), F(0))
+        b = (F(float(g.cap[gg])) - other) / (one_k * u)
+        best = b if best is None or b < best else best
+    ks = [k for k in range(w.K) if best is None or w.eta[k] <= best]
+    return (max(ks), True) if ks else (0, False)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_P13_block_step_is_exact_coordinate_minimisation(seed):
+    w = random_workload(seed=700 + seed, C=3, N=(20, 9, 14), L=50, K=8, M=9, E=1,
+                        with_groups=True, G=2)
+    S = oracle.S_exact(w)
+    W, _ = oracle.W_table(w, S)
+    k0 = oracle.bcd_init(w)
+    for c in range(w.C):
+        mean = F(int(w.samples_of(c).astype(np.int64).sum()), w.n_of(c))
+        assert w.eta[k0[c]] <= mean and (k0[c] == w.K - 1 or w.eta[k0[c] + 1] > mean)
+    out = oracle.bcd_step(w, W[0], k0)
+    kcur = list(k0)
+    for c in range(w.C):
+        kmax, feas = _feasible_kmax_exact(w, c, kcur)
+        assert bool(out["feasible"][c]) == feas
+        want = min(range(kmax + 1), key=lambda k: (W[0, c, k], k))
+        assert out["k_next"][c] == want
+        kcur[c] = want
+    # monotone decrease within a sweep from a feasible start
+    if all(out["feasible"]):
+        out2 = oracle.bcd_step(w, W[0], out["k_next"])
+        s1 = sum(W[0, c, out["k_next"][c]] for c in range(w.C))
+        s2 = sum(W[0, c, out2["k_next"][c]] for c in range(w.C))
+        assert s2 <= s1 + 1e-12 * abs(s1)
+    G = w.groups.G
+    for gg in range(G):
+        u = (1 + float(np.float32(w.groups.kappa))) * sum(
+            float(w.groups.conc[c * G + gg]) * int(w.eta[out["k_next"][c]]) for c in range(w.C))
+        assert abs(out["usage"][gg] - u) <= 1e-12 * max(1.0, u)
+
+
+# ---------------------------------------------------------------- P14 ------
+# Printed consequences of Prop. 4.2 (Sec. 5): rho = 10 reserves at about the
+# 91st percentile; rho = 20 at the 95th (Table 2: DRO equals P95 at rho = 20).
+
+def test_P14_paper_fractiles():
+    import json, os
+    path = os.path.join(os.path.dirname(__file__), "golden", "critical_fractile.json")
+    data = json.load(open(path))
+    N = 100_000
+    for row in data["rows"]:
+        rho = row["rho"]
+        j = oracle.rank(np.float32(rho), np.float32(1.0), N)
+        q = j / N
+        assert abs(q - row["q_star"]) <= 1.0 / N
+        if "printed_percentile" in row:
+            assert round(100 * q) == row["printed_percentile"]
+
+
+# ---------------------------------------------------------------- ties -----
+# Ties go to the lowest index.  Exact ties are structural: at eps = 0 every
+# multiplier at or above max(c_p, c_w) gives the SAA cost, and when q N is an
+# integer the SAA cost is flat between two order statistics.
+
+def test_ties_lowest_reservation_on_flat_saa():
+    xs = np.array([3, 9, 14, 20, 26, 31, 37, 44, 52, 60], np.int32)   # q = 4/5, q N = 8
+    L = 64
+    w = Workload("tie", 1, np.array([0, xs.size], np.int64), None, xs, np.array([L], np.int32),
+                 eta_grid(L + 1, L), lam_grid(9), np.array([4.0], np.float32),
+                 np.array([1.0], np.float32), 1, np.array([0.0], np.float32))
+    r = oracle.solve(w)
+    saa = [brute.saa_exact(int(e), xs.tolist(), 4.0, 1.0) for e in w.eta]
+    best = min(saa)
+    flat = [k for k, v in enumerate(saa) if v == best]
+    assert len(flat) > 1                                   # the flat stretch [x_(8), x_(9)]
+    assert r["k_star"][0, 0] == flat[0] == 44
+    assert r["q_value"][0] == 44 and r["q_rank"][0] == 8
+
+
+def test_ties_lowest_multiplier():
+    w = _tiny(81, E=1, N=(25, 12))
+    w.eps[:] = 0
+    r = oracle.solve(w)
+    S = r["S"]
+    for c in range(w.C):
+        xs = w.samples_of(c).tolist()
+        for k in range(w.K):
+            target = brute.saa_exact(int(w.eta[k]), xs, float(w.c_p[c]), float(w.c_w[c])) * len(xs)
+            first = next(m for m in range(w.M) if F(S.as_int((c, k, m)), 1 << 33) == target)
+            assert r["m_star"][0, c, k] == first

@@ -1,0 +1,326 @@
+"""Seeded synthetic stand-ins for the paper's output-length traces.
+
+The paper evaluates on production traces (BurstGPT, Azure LLM 2024, ShareGPT;
+Sec. 5.1 "Experiment Setup") that are not available here.  The five workloads
+below are synthetic, seeded and heavy-tailed, with the class counts, sample
+counts, grid sizes, radii and cost ratios of the benchmark configurations:
+
+  cfg1  1 class  x 1,000      lognormal(5, 1), clip [1, 4096]       K=64   M=32
+  cfg2  4 classes x 100,000   lognormal, means 50/300/1500/600       K=512  M=128
+  cfg3  16 classes x 1e6      2-component lognormal mixture + Pareto K=2048 M=256
+  cfg4  8 segments x 250,000, 16 cost ratios x 16 radii              K=1024 M=128
+  cfg5  8 classes x 4e6, mean drifting 1 %/iteration, 6 groups       K=2048 M=256
+
+Everything here is input generation: draws, rounding to integer lengths,
+the reservation and multiplier grids, radii as a fraction of the sample mean,
+and cost coefficients.  Nothing computes a cost, a dual, a quantile or an
+argmin.
+"""
+from __future__ import annotations
+
+import functools
+import math
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+
+CONFIG_NAMES = ("cfg1", "cfg2", "cfg3", "cfg4", "cfg5")
+
+# Sample lengths, grid points and support bounds are integers no larger than
+# 2**15; cost coefficients and multipliers lie in [2**-10, 2**7].
+MAX_LEN = 1 << 15
+
+
+@dataclass
+class Groups:
+    """Serving-group capacity data for one block step (eq. capacity)."""
+    cap: np.ndarray      # float32 [G]   KV capacity of each group, tokens
+    conc: np.ndarray     # float32 [C*G] expected concurrent class-c requests on group g
+    kappa: float         # safety factor (float32 value)
+
+    @property
+    def G(self) -> int:
+        return int(self.cap.shape[0])
+
+
+@dataclass
+class Workload:
+    name: str
+    C: int                       # classes (problem rows)
+    offsets: np.ndarray          # int64 [S+1] CSR bounds of the sample segments
+    seg: Optional[np.ndarray]    # int32 [C] segment of each class, None = identity
+    xi: np.ndarray               # int32 [offsets[-1]] output-length samples
+    L: np.ndarray                # int32 [C] support upper bound of each class
+    eta: np.ndarray              # int32 [K] ascending reservation (buffer) grid
+    lam: np.ndarray              # float32 [M] ascending multiplier grid
+    c_p: np.ndarray              # float32 [C] preemption cost per token
+    c_w: np.ndarray              # float32 [C] waste cost per token
+    E: int                       # radii per class
+    eps: np.ndarray              # float32 [E*C] Wasserstein radius, tokens, row e*C + c
+    groups: Optional[Groups] = None
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def K(self) -> int:
+        return int(self.eta.shape[0])
+
+    @property
+    def M(self) -> int:
+        return int(self.lam.shape[0])
+
+    @property
+    def S(self) -> int:
+        return int(self.offsets.shape[0] - 1)
+
+    def seg_of(self, c: int) -> int:
+        return c if self.seg is None else int(self.seg[c])
+
+    def n_of(self, c: int) -> int:
+        s = self.seg_of(c)
+        return int(self.offsets[s + 1] - self.offsets[s])
+
+    def samples_of(self, c: int) -> np.ndarray:
+        s = self.seg_of(c)
+        return self.xi[self.offsets[s]:self.offsets[s + 1]]
+
+    @property
+    def evals(self) -> int:
+        """Number of (class, grid point, multiplier, sample) terms."""
+        return sum(self.n_of(c) for c in range(self.C)) * self.K * self.M
+
+    def checksum(self) -> str:
+        """Content hash of every input array (detects generator drift)."""
+        import hashlib
+        h = hashlib.sha256()
+        for a in (self.offsets, self.xi, self.L, self.eta, self.lam, self.c_p, self.c_w, self.eps):
+            h.update(np.ascontiguousarray(a).tobytes())
+        if self.seg is not None:
+            h.update(np.ascontiguousarray(self.seg).tobytes())
+        if self.groups is not None:
+            h.update(self.groups.cap.tobytes())
+            h.update(self.groups.conc.tobytes())
+        return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------- grids ----
+
+def eta_grid(K: int, L: int) -> np.ndarray:
+    """K integer reservation levels spread uniformly over [0, L].
+
+    Point k is k*L/(K-1) rounded half-up, i.e. floor((2kL + K - 1) / (2(K-1))),
+    so the grid holds 0 and L and is strictly ascending whenever K - 1 <= L.
+    """
+    if K == 1:
+        return np.zeros(1, dtype=np.int32)
+    k = np.arange(K, dtype=np.int64)
+    return ((2 * k * L + K - 1) // (2 * (K - 1))).astype(np.int32)
+
+
+def lam_grid(M: int, lo: float = 1e-3, hi: float = 1e2) -> np.ndarray:
+    """M multipliers log-spaced on [lo, hi], each rounded once to float32."""
+    if M == 1:
+        return np.array([hi], dtype=np.float32)
+    a, b = math.log10(lo), math.log10(hi)
+    vals = [10.0 ** (a + (b - a) * m / (M - 1)) for m in range(M)]
+    return np.array(vals, dtype=np.float64).astype(np.float32)
+
+
+def _f32(v) -> np.ndarray:
+    return np.asarray(v, dtype=np.float64).astype(np.float32)
+
+
+def _clip_round(x: np.ndarray, lo: int, hi: int) -> np.ndarray:
+    """Round half-to-even to an integer length, then clip into [lo, hi]."""
+    return np.clip(np.rint(x), lo, hi).astype(np.int32)
+
+
+def _lognormal_by_mean(rng, mean: float, sigma: float, n: int) -> np.ndarray:
+    mu = math.log(mean) - 0.5 * sigma * sigma
+    return rng.lognormal(mu, sigma, n)
+
+
+def _csr(parts) -> tuple[np.ndarray, np.ndarray]:
+    offsets = np.zeros(len(parts) + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum([len(p) for p in parts])
+    xi = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
+    return offsets, xi
+
+
+def _mean(x: np.ndarray) -> float:
+    """Exact integer sum divided once (deterministic across machines)."""
+    return int(x.astype(np.int64).sum()) / len(x)
+
+
+# -------------------------------------------------------------- configs ----
+
+def _cfg1() -> Workload:
+    rng = np.random.default_rng(0)
+    L = 4096
+    x = _clip_round(rng.lognormal(5.0, 1.0, 1000), 1, L)
+    offsets, xi = _csr([x])
+    return Workload("cfg1", 1, offsets, None, xi, np.array([L], np.int32),
+                    eta_grid(64, L), lam_grid(32), _f32([8.0]), _f32([1.0]),
+                    1, _f32([10.0]),
+                    meta=dict(desc="1 class x 1,000 lognormal(5,1) lengths, clip [1,4096]"))
+
+
+def _cfg2() -> Workload:
+    rng = np.random.default_rng(1)
+    L = 8192
+    means, sig = (50.0, 300.0, 1500.0, 600.0), (0.8, 1.0, 1.2, 0.9)
+    parts = [_clip_round(_lognormal_by_mean(rng, m, s, 100_000), 1, L) for m, s in zip(means, sig)]
+    offsets, xi = _csr(parts)
+    eps = _f32([0.05 * _mean(p) for p in parts])
+    return Workload("cfg2", 4, offsets, None, xi, np.full(4, L, np.int32),
+                    eta_grid(512, L), lam_grid(128), _f32([4, 8, 16, 32]), _f32([1] * 4),
+                    1, eps,
+                    meta=dict(desc="4 classes x 1e5 lognormal lengths, clip [1,8192]"))
+
+
+def _cfg3() -> Workload:
+    rng = np.random.default_rng(2)
+    L, C, N = 32768, 16, 1_000_000
+    parts, cps = [], []
+    for _ in range(C):
+        m1, m2 = rng.uniform(20.0, 3000.0, 2)
+        comp = rng.random(N) < 0.7
+        a = _lognormal_by_mean(rng, m1, 1.0, N)
+        b = _lognormal_by_mean(rng, m2, 1.0, N)
+        x = np.where(comp, a, b)
+        tail = rng.random(N) < 0.02
+        xm = max(m1, m2)
+        x = np.where(tail, xm * (1.0 + rng.pareto(1.5, N)), x)
+        parts.append(_clip_round(x, 1, L))
+        cps.append(math.exp(rng.uniform(math.log(2.0), math.log(64.0))))
+    offsets, xi = _csr(parts)
+    eps = _f32([0.02 * _mean(p) for p in parts])
+    return Workload("cfg3", C, offsets, None, xi, np.full(C, L, np.int32),
+                    eta_grid(2048, L), lam_grid(256), _f32(cps), _f32([1.0] * C),
+                    1, eps,
+                    meta=dict(desc="16 classes x 1e6: 0.7/0.3 lognormal mixture (means U[20,3000], "
+                                   "sigma 1) + 2% Lomax(1.5) tail, clip [1,32768]"))
+
+
+def _cfg4() -> Workload:
+    """8 sample segments shared by 16 cost ratios: class c = ratio*8 + segment."""
+    rng = np.random.default_rng(3)
+    L, S, N, R, E = 32768, 8, 250_000, 16, 16
+    means = [40.0 * 100.0 ** (s / 7.0) for s in range(S)]
+    parts = [_clip_round(_lognormal_by_mean(rng, m, 1.0, N), 1, L) for m in means]
+    offsets, xi = _csr(parts)
+    C = R * S
+    seg = np.array([c % S for c in range(C)], np.int32)
+    rho = [128.0 ** (i / 15.0) for i in range(R)]
+    c_w = _f32([0.5] * C)
+    c_p = _f32([0.5 * rho[c // S] for c in range(C)])
+    smean = [_mean(p) for p in parts]
+    eps = np.empty(E * C, np.float32)
+    for e in range(E):
+        for c in range(C):
+            eps[e * C + c] = np.float32(0.2 * smean[c % S] * e / 15.0)
+    return Workload("cfg4", C, offsets, seg, xi, np.full(C, L, np.int32),
+                    eta_grid(1024, L), lam_grid(128), c_p, c_w, E, eps,
+                    meta=dict(desc="8 segments x 2.5e5 lognormal (means 40..4000), "
+                                   "x 16 ratios in [1,128] x 16 radii in [0, 0.2 mean]",
+                              rho=rho))
+
+
+@functools.lru_cache(maxsize=1)
+def _cfg5_base():
+    rng = np.random.default_rng(4)
+    C, N, G = 8, 4_000_000, 6
+    means = [40.0 * 100.0 ** (c / 7.0) for c in range(C)]
+    base = [_lognormal_by_mean(rng, m, 1.0, N) for m in means]
+    cps = [math.exp(rng.uniform(math.log(2.0), math.log(64.0))) for _ in range(C)]
+    cap = rng.uniform(20_000.0, 400_000.0, G)
+    mask = rng.random((C, G)) < 0.5
+    for c in range(C):
+        if not mask[c].any():
+            mask[c, rng.integers(G)] = True
+    conc = np.where(mask, rng.uniform(0.5, 4.0, (C, G)), 0.0)
+    return base, cps, cap, conc
+
+
+def _cfg5(iteration: int = 0) -> Workload:
+    base, cps, cap, conc = _cfg5_base()
+    L, C = 32768, 8
+    drift = 1.01 ** iteration
+    parts = [_clip_round(b * drift, 1, L) for b in base]
+    offsets, xi = _csr(parts)
+    eps = _f32([0.02 * _mean(p) for p in parts])
+    groups = Groups(_f32(cap), _f32(conc.reshape(-1)), float(np.float32(0.2)))
+    return Workload("cfg5", C, offsets, None, xi, np.full(C, L, np.int32),
+                    eta_grid(2048, L), lam_grid(256), _f32(cps), _f32([1.0] * C),
+                    1, eps, groups=groups,
+                    meta=dict(desc="8 classes x 4e6 lognormal (means 40..4000) drifting 1%/iteration; "
+                                   "6 groups, capacities U[20k,400k]", iteration=iteration))
+
+
+def make_workload(name: str, **kw) -> Workload:
+    if name == "cfg1":
+        return _cfg1()
+    if name == "cfg2":
+        return _cfg2()
+    if name == "cfg3":
+        return _cfg3()
+    if name == "cfg4":
+        return _cfg4()
+    if name == "cfg5":
+        return _cfg5(kw.get("iteration", 0))
+    if name == "random":
+        return random_workload(**kw)
+    raise ValueError(f"unknown workload {name!r}")
+
+
+def random_workload(seed: int = 0, C: int = 3, N=(50, 7, 130), L: int = 300, K: int = 16,
+                    M: int = 12, E: int = 2, lam_lo: float = 1e-3, lam_hi: float = 1e2,
+                    cost_choices=None, alias: bool = False, with_groups: bool = False,
+                    G: int = 2, dist: str = "lognormal") -> Workload:
+    """Small ragged workload for parity and property tests.
+
+    N may be an int or a per-segment tuple (ragged segments).  With `alias`,
+    classes share segments (seg[c] = c % S with S = len(N)).
+    """
+    rng = np.random.default_rng(seed)
+    Ns = [N] * C if isinstance(N, int) else list(N)
+    S = len(Ns)
+    parts = []
+    for s, n in enumerate(Ns):
+        if dist == "lognormal":
+            mean = float(rng.uniform(0.05, 0.6) * L)
+            x = _clip_round(_lognormal_by_mean(rng, mean, float(rng.uniform(0.3, 1.3)), n), 0, L)
+        elif dist == "uniform":
+            x = rng.integers(0, L + 1, n).astype(np.int32)
+        elif dist == "constant":
+            x = np.full(n, int(rng.integers(0, L + 1)), np.int32)
+        else:
+            raise ValueError(dist)
+        parts.append(x)
+    offsets, xi = _csr(parts)
+    if alias:
+        seg = np.array([c % S for c in range(C)], np.int32)
+    else:
+        if S != C:
+            raise ValueError("without aliasing there must be one segment per class")
+        seg = None
+    if cost_choices is None:
+        c_p = _f32(np.exp(rng.uniform(math.log(0.5), math.log(64.0), C)))
+        c_w = _f32(np.exp(rng.uniform(math.log(0.25), math.log(4.0), C)))
+    else:
+        c_p = _f32([cost_choices[int(i)][0] for i in rng.integers(len(cost_choices), size=C)])
+        c_w = _f32([cost_choices[int(i)][1] for i in rng.integers(len(cost_choices), size=C)])
+    eps = _f32(rng.uniform(0.0, 0.2 * L, E * C))
+    if E * C:
+        eps[: min(C, E * C)] = 0.0     # one radius row at exactly zero
+    groups = None
+    if with_groups:
+        conc = np.where(rng.random((C, G)) < 0.6, rng.uniform(0.5, 4.0, (C, G)), 0.0)
+        for c in range(C):
+            if not (conc[c] > 0).any():
+                conc[c, rng.integers(G)] = float(rng.uniform(0.5, 4.0))
+        cap = rng.uniform(0.3, 2.0, G) * L * C
+        groups = Groups(_f32(cap), _f32(conc.reshape(-1)), float(np.float32(0.2)))
+    return Workload(f"random{seed}", C, offsets, seg, xi, np.full(C, L, np.int32),
+                    eta_grid(K, L), lam_grid(M, lam_lo, lam_hi), c_p, c_w, E, eps,
+                    groups=groups, meta=dict(desc=f"random seed={seed}"))
