@@ -1,0 +1,67 @@
+"""ctypes view of libdro.so (include/dro.h).  Argument marshalling only."""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+import threading
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdro.so")
+
+_lock = threading.Lock()
+_lib = None
+
+P = ct.c_void_p
+i32 = ct.c_int32
+
+
+class ProblemStruct(ct.Structure):
+    _fields_ = [("C", i32), ("S", i32), ("offsets", P), ("offsets_h", P), ("seg", P), ("seg_h", P),
+                ("xi", P), ("L", P), ("K", i32), ("eta", P), ("M", i32), ("lam", P), ("c_p", P),
+                ("c_w", P)]
+
+
+class GroupsStruct(ct.Structure):
+    _fields_ = [("G", i32), ("cap", P), ("conc", P), ("kappa", ct.c_float)]
+
+
+class StepOutStruct(ct.Structure):
+    _fields_ = [("k_next", P), ("W_star", P), ("q_value", P), ("usage", P), ("feasible", P)]
+
+
+EXPORTS = {
+    "dro_strerror": (ct.c_char_p, [ct.c_int]),
+    "dro_create": (ct.c_int, [ct.c_int, ct.POINTER(P)]),
+    "dro_destroy": (None, [P]),
+    "dro_last_error": (ct.c_char_p, [P]),
+    "dro_validate": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P]),
+    "dro_take_flags": (ct.c_int, [P, ct.POINTER(ct.c_uint32)]),
+    "dro_cost_eval": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P]),
+    "dro_argmin_reservation": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P, P, P]),
+    "class_quantile": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P, P]),
+    "bcd_init_state": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P]),
+    "bcd_block_step": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, ct.POINTER(GroupsStruct), P,
+                                  ct.POINTER(StepOutStruct), P]),
+}
+
+
+class NativeMissing(RuntimeError):
+    pass
+
+
+def load():
+    """The loaded library; raises NativeMissing if libdro.so was not built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise NativeMissing(
+                    f"{LIB_PATH} is missing: build it with `python -m paper_2607_16892_amd.build` "
+                    "(the reservation path has no fallback)")
+            lib = ct.CDLL(LIB_PATH)
+            for name, (res, args) in EXPORTS.items():
+                fn = getattr(lib, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = lib
+    return _lib

@@ -1,0 +1,133 @@
+// Internal declarations shared by the HIP translation units of libdro.
+// Not part of the public ABI (include/dro.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dro.h"
+
+namespace dro {
+
+// ---- dense evaluation -------------------------------------------------------
+// Every lane owns a register tile of TK grid points x TM multipliers; a
+// 256-lane block covers (TK * lanes_k) x (TM * lanes_m) pairs of one class and
+// one slice of that class's samples, staged through LDS.
+constexpr int kThreads = 256;
+constexpr int kTK = 4;
+constexpr int kTM = 8;
+constexpr int kTileN = 1024;  // samples staged per LDS tile
+constexpr int kRun = 64;      // fp32 run length before the fp64 fold
+
+struct DensePlan {
+    int lanes_m, lanes_k;  // lane grid inside a block
+    int tiles_k, tiles_m;  // block tiles per class
+    int P;                 // sample slices per class
+    long long blocks;      // C * tiles_k * tiles_m * P
+};
+
+struct DenseArgs {
+    const int64_t *offsets;
+    const int32_t *seg;
+    const int32_t *xi;
+    const int32_t *L;
+    const int32_t *eta;
+    const float *lam;
+    const float *c_p;
+    const float *c_w;
+    int C, K, M;
+    DensePlan plan;
+    double *out;  // [P][C][K][M]; with P == 1 this is S itself
+};
+
+hipError_t launch_dense(const DenseArgs &a, hipStream_t st);
+// S[i] = sum_p part[p * n + i], p ascending
+hipError_t launch_reduce_slices(const double *part, int P, long long n, double *S, hipStream_t st);
+// W[e,c,k] = min_m RN(RN(lam_m eps[e,c]) + RN(S[c,k,m] / N_c)), lowest m
+hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const int32_t *seg,
+                                  const float *lam, const float *eps, int E, int C, int K, int M,
+                                  double *W, int32_t *m_star, hipStream_t st);
+
+// ---- exact screening / refine ----------------------------------------------
+constexpr int kBandCap = 256;     // candidates kept per (e, c)
+constexpr double kBandTau = 1e-4; // relative width of the screening band
+
+struct BandArgs {
+    const double *S;  // approximate [C][K][M]
+    const int64_t *offsets;
+    const int32_t *seg;
+    const int32_t *L;
+    const float *lam;
+    const float *c_p;
+    const float *c_w;
+    const float *eps;     // [E][C]
+    const int32_t *k_max; // [C] or null
+    int E, C, K, M;
+    int e_row, c_only;    // c_only >= 0: one (e_row, c_only) problem only
+    int32_t *cand;        // [EC][kBandCap] packed k * M + m
+    int32_t *count;       // [EC]
+    double *thresh;       // [EC]
+    uint32_t *flags;
+};
+hipError_t launch_band(const BandArgs &a, hipStream_t st);
+
+struct RefineArgs {
+    const int64_t *offsets;
+    const int32_t *seg;
+    const int32_t *xi;
+    const int32_t *L;
+    const int32_t *eta;
+    const float *lam;
+    const float *c_p;
+    const float *c_w;
+    const int32_t *cand;
+    const int32_t *count;
+    int C, M, EC, P;
+    int e_row, c_only;
+    uint64_t *part;  // [EC][kBandCap][P][2] (lo, hi) exact partial sums
+};
+hipError_t launch_refine(const RefineArgs &a, hipStream_t st);
+
+struct FinalArgs {
+    const int64_t *offsets;
+    const int32_t *seg;
+    const float *lam;
+    const float *eps;
+    const int32_t *cand;
+    const int32_t *count;
+    const double *thresh;
+    const uint64_t *part;
+    int C, M, EC, P;
+    int e_row, c_only;
+    int32_t *k_star;
+    double *W_star;
+    int32_t *m_at_star;
+    uint32_t *flags;
+};
+hipError_t launch_finalize(const FinalArgs &a, hipStream_t st);
+
+// ---- quantile ----------------------------------------------------------------
+constexpr int kHistBins = 32769;   // values 0 .. 2^15
+constexpr int kHistChunk = 65535;  // samples per block (16-bit LDS counters)
+hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st);
+hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, long long max_seg,
+                            uint32_t *hist, hipStream_t st);
+hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
+                         const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
+                         int64_t *q_rank, hipStream_t st);
+
+// ---- block step ----------------------------------------------------------------
+hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
+                           const int32_t *eta, int C, int K, int32_t *k0, hipStream_t st);
+hipError_t launch_bcd_kmax(const int32_t *eta, int C, int K, int G, const float *cap,
+                           const float *conc, float kappa, const int32_t *kcur, int c,
+                           int32_t *kmax, uint8_t *feasible, hipStream_t st);
+hipError_t launch_bcd_finish(const int32_t *eta, int C, int K, int G, const float *conc,
+                             float kappa, const int32_t *kcur, double *usage, int32_t *k_next,
+                             hipStream_t st);
+
+// ---- validation ----------------------------------------------------------------
+hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, int32_t *mn,
+                             int32_t *mx, hipStream_t st);
+
+}  // namespace dro

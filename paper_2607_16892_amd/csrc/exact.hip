@@ -1,0 +1,515 @@
+// Exact parts of the reservation path: the screened argmin refine, the
+// critical-fractile quantile, the block-step sweep and device-data checks.
+//
+// Compiled with -ffp-contract=off: every double expression below is the
+// round-to-nearest-even sequence written, with no fused multiply-add.
+//
+// Fixed point.  Inside the library's limits (integers <= 2^15, binary32
+// coefficients in [2^-10, 2^7]) every candidate of phi (Appendix A, Step 4)
+// is an integer multiple of 2^-33 below 2^56, so phi is evaluated exactly in
+// 64-bit integers and summed exactly in 128-bit integers.  The reported value
+// is J = RN(RN(lam eps) + RN(RN(S) / N)) with RN(S) the correctly rounded
+// double of the exact sum.
+#include "dro_internal.h"
+
+namespace dro {
+
+__device__ __forceinline__ int seg_of_x(const int32_t *seg, int c) { return seg ? seg[c] : c; }
+
+// v * 2^33 for a binary32 v in [2^-10, 2^7] (exact integer below 2^41).
+__device__ __forceinline__ int64_t fix33(float v)
+{
+    const uint32_t bits = __float_as_uint(v);
+    const int e = (int)((bits >> 23) & 0xffu);
+    const int64_t mant = (int64_t)((bits & 0x7fffffu) | 0x800000u);
+    const int sh = e - 117;  // e - 127 - 23 + 33
+    return sh >= 0 ? (mant << sh) : (mant >> (-sh));
+}
+
+// phi in units of 2^-33: the three candidate points 0, x and L of Step 4.
+__device__ __forceinline__ int64_t phi_fix(int64_t eta, int64_t x, int64_t L, int64_t CP,
+                                           int64_t CW, int64_t G)
+{
+    const int64_t d = x - eta;
+    const int64_t q_x = d > 0 ? CP * d : CW * (-d);  // c_p (x-eta)^+ + c_w (eta-x)^+
+    const int64_t q_0 = CW * eta - G * x;            // Q(eta, 0) - g x
+    const int64_t q_L = CP * (L - eta) - G * (L - x);// Q(eta, L) - g (L - x)
+    const int64_t m = q_0 > q_L ? q_0 : q_L;
+    return q_x > m ? q_x : m;
+}
+
+// Correctly rounded double of the unsigned 128-bit value (hi, lo) times 2^-33.
+__device__ double fix128_to_double(uint64_t lo, uint64_t hi)
+{
+    int nb;
+    if (hi) nb = 128 - __clzll((long long)hi);
+    else if (lo) nb = 64 - __clzll((long long)lo);
+    else return 0.0;
+    if (nb <= 53) return ldexp((double)(long long)lo, -33);
+    const int sh = nb - 53;
+    const unsigned __int128 v = ((unsigned __int128)hi << 64) | (unsigned __int128)lo;
+    uint64_t mant = (uint64_t)(v >> sh);
+    const unsigned __int128 rem = v & ((((unsigned __int128)1) << sh) - 1);
+    const unsigned __int128 half = ((unsigned __int128)1) << (sh - 1);
+    if (rem > half || (rem == half && (mant & 1u))) mant += 1;
+    return ldexp((double)(long long)mant, sh - 33);
+}
+
+__device__ __forceinline__ void add128(uint64_t &lo, uint64_t &hi, uint64_t blo, uint64_t bhi)
+{
+    const uint64_t r = lo + blo;
+    hi += bhi + (r < lo ? 1u : 0u);
+    lo = r;
+}
+
+// ------------------------------------------------------------------ band ----
+// Block per (e, c).  Screens every (k <= kmax, m) by the approximate dual value
+// and keeps those within a relative band of the approximate minimum.  For
+// lam_m >= max(c_p, c_w) every sample keeps its own point, so S is the SAA sum
+// for all such m and J can only grow with m: only the first of them can be a
+// lowest-index minimiser, and the others are not screened.
+__global__ __launch_bounds__(256) void band_kernel(BandArgs a)
+{
+    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
+    const int e = ec / a.C, c = ec % a.C;
+    const int t = threadIdx.x;
+    const int s = seg_of_x(a.seg, c);
+    const double N = (double)(a.offsets[s + 1] - a.offsets[s]);
+    const float cp = a.c_p[c], cw = a.c_w[c];
+    const float top = cp > cw ? cp : cw;
+
+    __shared__ int s_mfirst;
+    __shared__ double s_min[256];
+    __shared__ int s_count;
+    if (t == 0) {
+        int mf = a.M - 1;
+        for (int m = 0; m < a.M; ++m)
+            if (a.lam[m] >= top) { mf = m; break; }
+        s_mfirst = mf;
+        s_count = 0;
+    }
+    __syncthreads();
+    const int mlim = s_mfirst;
+    int kmax = a.K - 1;
+    if (a.k_max) {
+        kmax = a.k_max[c];
+        kmax = kmax < 0 ? 0 : (kmax > a.K - 1 ? a.K - 1 : kmax);
+    }
+    const double ev = (double)a.eps[(long long)e * a.C + c];
+    const long long npair = (long long)(kmax + 1) * (mlim + 1);
+    const double *Sc = a.S + (long long)c * a.K * a.M;
+
+    double lmin = __builtin_inf();
+    for (long long i = t; i < npair; i += 256) {
+        const int k = (int)(i / (mlim + 1)), m = (int)(i % (mlim + 1));
+        const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
+                                   __ddiv_rn(Sc[(long long)k * a.M + m], N));
+        lmin = J < lmin ? J : lmin;
+    }
+    s_min[t] = lmin;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) s_min[t] = s_min[t + w] < s_min[t] ? s_min[t + w] : s_min[t];
+        __syncthreads();
+    }
+    const double wmin = s_min[0];
+    const double slack = 1e-12 * (double)(cp + cw) * (double)a.L[c];
+    const double T = wmin + kBandTau * wmin + slack;
+
+    for (long long i = t; i < npair; i += 256) {
+        const int k = (int)(i / (mlim + 1)), m = (int)(i % (mlim + 1));
+        const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
+                                   __ddiv_rn(Sc[(long long)k * a.M + m], N));
+        if (J <= T) {
+            const int slot = atomicAdd(&s_count, 1);
+            if (slot < kBandCap) a.cand[(long long)ec * kBandCap + slot] = k * a.M + m;
+        }
+    }
+    __syncthreads();
+    if (t == 0) {
+        int n = s_count;
+        if (n > kBandCap) {
+            atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_FULL);
+            n = kBandCap;
+        }
+        a.count[ec] = n;
+        a.thresh[ec] = T;
+    }
+}
+
+hipError_t launch_band(const BandArgs &a, hipStream_t st)
+{
+    const int blocks = a.c_only >= 0 ? 1 : a.E * a.C;
+    hipLaunchKernelGGL(band_kernel, dim3(blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- refine ----
+// Block (slice p, problem ec): exact partial sums of phi over slice p of the
+// class's samples, for every screened candidate of ec.
+__global__ __launch_bounds__(256) void refine_kernel(RefineArgs a)
+{
+    const int p = blockIdx.y;
+    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
+    const int c = ec % a.C;
+    const int t = threadIdx.x;
+    const int s = seg_of_x(a.seg, c);
+    const long long n0 = a.offsets[s], N = a.offsets[s + 1] - n0;
+    const long long lo = n0 + (N * p) / a.P, hi = n0 + (N * (p + 1)) / a.P;
+    const int64_t CP = fix33(a.c_p[c]), CW = fix33(a.c_w[c]);
+    const int64_t L = a.L[c];
+    const int cnt = a.count[ec];
+
+    __shared__ uint64_t s_lo[256], s_hi[256];
+    for (int i = 0; i < cnt; ++i) {
+        const int packed = a.cand[(long long)ec * kBandCap + i];
+        const int k = packed / a.M, m = packed % a.M;
+        const int64_t eta = a.eta[k];
+        const int64_t G = fix33(a.lam[m]);
+        uint64_t alo = 0, ahi = 0;
+        for (long long n = lo + t; n < hi; n += 256) {
+            const uint64_t v = (uint64_t)phi_fix(eta, a.xi[n], L, CP, CW, G);
+            add128(alo, ahi, v, 0);
+        }
+        s_lo[t] = alo;
+        s_hi[t] = ahi;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (t < w) {
+                uint64_t l = s_lo[t], h = s_hi[t];
+                add128(l, h, s_lo[t + w], s_hi[t + w]);
+                s_lo[t] = l;
+                s_hi[t] = h;
+            }
+            __syncthreads();
+        }
+        if (t == 0) {
+            uint64_t *o = a.part + (((long long)ec * kBandCap + i) * a.P + p) * 2;
+            o[0] = s_lo[0];
+            o[1] = s_hi[0];
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_refine(const RefineArgs &a, hipStream_t st)
+{
+    const int xs = a.c_only >= 0 ? 1 : a.EC;
+    hipLaunchKernelGGL(refine_kernel, dim3(xs, a.P), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// -------------------------------------------------------------- finalize ----
+// Block per ec: exact S and J of every candidate, then the lowest (k, m) with
+// the smallest J (candidates are packed k * M + m, so one integer orders them).
+__global__ __launch_bounds__(256) void finalize_kernel(FinalArgs a)
+{
+    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
+    const int e = ec / a.C, c = ec % a.C;
+    const int t = threadIdx.x;
+    const int s = seg_of_x(a.seg, c);
+    const double N = (double)(a.offsets[s + 1] - a.offsets[s]);
+    const double ev = (double)a.eps[(long long)e * a.C + c];
+    const int cnt = a.count[ec];
+
+    double bJ = __builtin_inf();
+    int bkey = 0x7fffffff;
+    for (int i = t; i < cnt; i += 256) {
+        uint64_t lo = 0, hi = 0;
+        const uint64_t *pp = a.part + ((long long)ec * kBandCap + i) * a.P * 2;
+        for (int p = 0; p < a.P; ++p) add128(lo, hi, pp[2 * p], pp[2 * p + 1]);
+        const int key = a.cand[(long long)ec * kBandCap + i];
+        const int m = key % a.M;
+        const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
+                                   __ddiv_rn(fix128_to_double(lo, hi), N));
+        if (J < bJ || (J == bJ && key < bkey)) {
+            bJ = J;
+            bkey = key;
+        }
+    }
+    __shared__ double sJ[256];
+    __shared__ int sK[256];
+    sJ[t] = bJ;
+    sK[t] = bkey;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) {
+            const double j2 = sJ[t + w];
+            const int k2 = sK[t + w];
+            if (j2 < sJ[t] || (j2 == sJ[t] && k2 < sK[t])) {
+                sJ[t] = j2;
+                sK[t] = k2;
+            }
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        const int key = sK[0];
+        a.k_star[ec] = key / a.M;
+        a.W_star[ec] = sJ[0];
+        if (a.m_at_star) a.m_at_star[ec] = key % a.M;
+        // the exact optimum must sit well inside the screening band
+        const double T = a.thresh[ec];
+        if (!(sJ[0] * (1.0 + 0.5 * kBandTau) < T) || cnt == 0) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_MARGIN);
+    }
+}
+
+hipError_t launch_finalize(const FinalArgs &a, hipStream_t st)
+{
+    const int blocks = a.c_only >= 0 ? 1 : a.EC;
+    hipLaunchKernelGGL(finalize_kernel, dim3(blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// -------------------------------------------------------------- quantile ----
+__global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
+{
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
+{
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n, v);
+    return hipGetLastError();
+}
+
+// Block (chunk, segment): counts of the values 0 .. 2^15 - 1 of up to
+// kHistChunk samples, two 16-bit counters per LDS word, flushed to the
+// segment's global histogram; the value 2^15 goes straight to global memory.
+__global__ __launch_bounds__(256) void histogram_kernel(const int64_t *offsets, const int32_t *xi,
+                                                        uint32_t *hist, int chunks)
+{
+    constexpr int kWords = (kHistBins - 1) / 2;
+    __shared__ uint32_t h[kWords];
+    const int s = (int)(blockIdx.x / chunks);
+    const long long chunk = blockIdx.x % chunks;
+    const long long n0 = offsets[s], n1 = offsets[s + 1];
+    const long long lo = n0 + chunk * kHistChunk;
+    if (lo >= n1) return;
+    const long long hi = min(n1, lo + kHistChunk);
+    uint32_t *g = hist + (long long)s * kHistBins;
+    for (int i = threadIdx.x; i < kWords; i += 256) h[i] = 0;
+    __syncthreads();
+    for (long long n = lo + threadIdx.x; n < hi; n += 256) {
+        int v = xi[n];
+        v = v < 0 ? 0 : (v > kHistBins - 1 ? kHistBins - 1 : v);
+        if (v == kHistBins - 1) atomicAdd(&g[v], 1u);
+        else atomicAdd(&h[v >> 1], 1u << ((v & 1) * 16));
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kWords; i += 256) {
+        const uint32_t w = h[i];
+        if (w & 0xffffu) atomicAdd(&g[2 * i], w & 0xffffu);
+        if (w >> 16) atomicAdd(&g[2 * i + 1], w >> 16);
+    }
+}
+
+hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, long long max_seg,
+                            uint32_t *hist, hipStream_t st)
+{
+    const long long chunks = (max_seg + kHistChunk - 1) / kHistChunk;
+    if (chunks <= 0 || S <= 0) return hipSuccess;
+    hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)(chunks * S)), dim3(256), 0, st, offsets,
+                       xi, hist, (int)chunks);
+    return hipGetLastError();
+}
+
+// Exact rank j = ceil(c_p N / (c_p + c_w)) in [1, N]: estimate in double,
+// then correct with exact 128-bit products.
+__device__ int64_t exact_rank(float cp, float cw, int64_t N)
+{
+    const uint64_t P = (uint64_t)fix33(cp), Wc = (uint64_t)fix33(cw);
+    const uint64_t den = P + Wc;
+    const unsigned __int128 num = (unsigned __int128)P * (uint64_t)N;
+    int64_t j = (int64_t)ceil((double)P / (double)den * (double)N);
+    if (j < 1) j = 1;
+    if (j > N) j = N;
+    while (j > 1 && (unsigned __int128)(uint64_t)(j - 1) * den >= num) --j;
+    while (j < N && (unsigned __int128)(uint64_t)j * den < num) ++j;
+    return j;
+}
+
+// Block per class: prefix counts over the segment histogram; the j-th
+// smallest sample is the first value whose cumulative count reaches j.
+__global__ __launch_bounds__(256) void select_kernel(const int64_t *offsets, const int32_t *seg,
+                                                     const float *c_p, const float *c_w,
+                                                     const uint32_t *hist, int32_t *q_value,
+                                                     int64_t *q_rank)
+{
+    const int c = blockIdx.x, t = threadIdx.x;
+    const int s = seg_of_x(seg, c);
+    const int64_t N = offsets[s + 1] - offsets[s];
+    const int64_t j = exact_rank(c_p[c], c_w[c], N);
+    const uint32_t *h = hist + (long long)s * kHistBins;
+    constexpr int per = (kHistBins + 255) / 256;
+    const int b0 = t * per, b1 = min(kHistBins, b0 + per);
+    uint64_t part = 0;
+    for (int v = b0; v < b1; ++v) part += h[v];
+    __shared__ uint64_t sc[256];
+    sc[t] = part;
+    __syncthreads();
+    for (int w = 1; w < 256; w <<= 1) {  // inclusive scan
+        const uint64_t add = t >= w ? sc[t - w] : 0;
+        __syncthreads();
+        sc[t] += add;
+        __syncthreads();
+    }
+    const uint64_t before = sc[t] - part;
+    if ((int64_t)before < j && j <= (int64_t)sc[t]) {
+        uint64_t cum = before;
+        for (int v = b0; v < b1; ++v) {
+            cum += h[v];
+            if ((int64_t)cum >= j) {
+                q_value[c] = v;
+                break;
+            }
+        }
+    }
+    if (t == 0) q_rank[c] = j;
+}
+
+hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
+                         const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
+                         int64_t *q_rank, hipStream_t st)
+{
+    hipLaunchKernelGGL(select_kernel, dim3(C), dim3(256), 0, st, offsets, seg, c_p, c_w, hist,
+                       q_value, q_rank);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ block step ----
+// Grid indices arriving from the caller (k_prev) are clamped into [0, K).
+__device__ __forceinline__ int clampk(int k, int K) { return k < 0 ? 0 : (k >= K ? K - 1 : k); }
+
+// Alg. 1 initialisation: largest k with eta[k] * N <= sum of the samples.
+__global__ __launch_bounds__(256) void bcd_init_kernel(const int64_t *offsets, const int32_t *seg,
+                                                       const int32_t *xi, const int32_t *eta, int K,
+                                                       int32_t *k0)
+{
+    const int c = blockIdx.x, t = threadIdx.x;
+    const int s = seg_of_x(seg, c);
+    const long long n0 = offsets[s], n1 = offsets[s + 1];
+    long long sum = 0;
+    for (long long n = n0 + t; n < n1; n += 256) sum += xi[n];
+    __shared__ long long sh[256];
+    sh[t] = sum;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) sh[t] += sh[t + w];
+        __syncthreads();
+    }
+    if (t == 0) {
+        const long long tot = sh[0], N = n1 - n0;
+        int best = 0;
+        for (int k = 0; k < K; ++k)
+            if ((long long)eta[k] * N <= tot) best = k;
+        k0[c] = best;
+    }
+}
+
+hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
+                           const int32_t *eta, int C, int K, int32_t *k0, hipStream_t st)
+{
+    hipLaunchKernelGGL(bcd_init_kernel, dim3(C), dim3(256), 0, st, offsets, seg, xi, eta, K, k0);
+    return hipGetLastError();
+}
+
+// Capacity bound of class c (eq. capacity), then the largest admissible k.
+__global__ void bcd_kmax_kernel(const int32_t *eta, int C, int K, int G, const float *cap,
+                                const float *conc, float kappa, const int32_t *kcur, int c,
+                                int32_t *kmax, uint8_t *feasible)
+{
+    if (threadIdx.x != 0) return;
+    const double onek = __dadd_rn(1.0, (double)kappa);
+    double bound = __builtin_inf();
+    for (int g = 0; g < G; ++g) {
+        const double u = (double)conc[c * G + g];
+        if (!(u > 0.0)) continue;
+        double sum = 0.0;
+        for (int c2 = 0; c2 < C; ++c2) {
+            if (c2 == c) continue;
+            sum = __dadd_rn(sum, __dmul_rn((double)conc[c2 * G + g], (double)eta[clampk(kcur[c2], K)]));
+        }
+        const double other = __dmul_rn(onek, sum);
+        const double num = __dsub_rn((double)cap[g], other);
+        const double den = __dmul_rn(onek, u);
+        const double b = __ddiv_rn(num, den);
+        bound = b < bound ? b : bound;
+    }
+    int km = -1;
+    for (int k = 0; k < K; ++k)
+        if ((double)eta[k] <= bound) km = k;
+    feasible[c] = km >= 0 ? 1 : 0;
+    kmax[c] = km >= 0 ? km : 0;
+}
+
+hipError_t launch_bcd_kmax(const int32_t *eta, int C, int K, int G, const float *cap,
+                           const float *conc, float kappa, const int32_t *kcur, int c,
+                           int32_t *kmax, uint8_t *feasible, hipStream_t st)
+{
+    hipLaunchKernelGGL(bcd_kmax_kernel, dim3(1), dim3(64), 0, st, eta, C, K, G, cap, conc, kappa,
+                       kcur, c, kmax, feasible);
+    return hipGetLastError();
+}
+
+__global__ void bcd_finish_kernel(const int32_t *eta, int C, int K, int G, const float *conc,
+                                  float kappa, const int32_t *kcur, double *usage, int32_t *k_next)
+{
+    const int t = threadIdx.x;
+    const double onek = __dadd_rn(1.0, (double)kappa);
+    for (int g = t; g < G; g += blockDim.x) {
+        double sum = 0.0;
+        for (int c = 0; c < C; ++c)
+            sum = __dadd_rn(sum, __dmul_rn((double)conc[c * G + g], (double)eta[clampk(kcur[c], K)]));
+        usage[g] = __dmul_rn(onek, sum);
+    }
+    for (int c = t; c < C; c += blockDim.x) k_next[c] = clampk(kcur[c], K);
+}
+
+hipError_t launch_bcd_finish(const int32_t *eta, int C, int K, int G, const float *conc,
+                             float kappa, const int32_t *kcur, double *usage, int32_t *k_next,
+                             hipStream_t st)
+{
+    hipLaunchKernelGGL(bcd_finish_kernel, dim3(1), dim3(256), 0, st, eta, C, K, G, conc, kappa,
+                       kcur, usage, k_next);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ validation ----
+__global__ __launch_bounds__(256) void seg_minmax_kernel(const int64_t *offsets, const int32_t *xi,
+                                                         int32_t *mn, int32_t *mx)
+{
+    const int s = blockIdx.x, t = threadIdx.x;
+    int a = 0x7fffffff, b = -0x7fffffff - 1;
+    for (long long n = offsets[s] + t; n < offsets[s + 1]; n += 256) {
+        const int v = xi[n];
+        a = v < a ? v : a;
+        b = v > b ? v : b;
+    }
+    __shared__ int sa[256], sb[256];
+    sa[t] = a;
+    sb[t] = b;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) {
+            sa[t] = sa[t + w] < sa[t] ? sa[t + w] : sa[t];
+            sb[t] = sb[t + w] > sb[t] ? sb[t + w] : sb[t];
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        mn[s] = sa[0];
+        mx[s] = sb[0];
+    }
+}
+
+hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, int32_t *mn,
+                             int32_t *mx, hipStream_t st)
+{
+    hipLaunchKernelGGL(seg_minmax_kernel, dim3(S), dim3(256), 0, st, offsets, xi, mn, mx);
+    return hipGetLastError();
+}
+
+}  // namespace dro

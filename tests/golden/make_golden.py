@@ -1,0 +1,83 @@
+"""Write the stored oracle results of the benchmark workloads.
+
+    python tests/golden/make_golden.py cfg1 cfg2 cfg3 cfg4 [cfg5:ITERS]
+
+Calls only `oracle/` (exact 128-bit evaluation, value-grouped) and the seeded
+generator in `workloads/`.  Each file records the generator checksum of its
+inputs, so a test can tell a changed input from a wrong result.  Doubles are
+stored as hex strings (bit-exact).
+"""
+from __future__ import annotations
+
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+from workloads import make_workload  # noqa: E402
+
+
+def _hex(a):
+    return [[float(v).hex() for v in row] for row in np.asarray(a, np.float64)]
+
+
+def golden_static(name: str) -> dict:
+    w = make_workload(name)
+    t0 = time.time()
+    r = oracle.solve(w, grouped=True)
+    out = dict(workload=name, checksum=w.checksum(), oracle_seconds=round(time.time() - t0, 1),
+               oracle_threads=oracle.threads(),
+               k_star=r["k_star"].tolist(), W_star=_hex(r["W_star"]),
+               m_at_star=r["m_at_star"].tolist(), q_value=r["q_value"].tolist(),
+               q_rank=r["q_rank"].tolist(),
+               # a few full W rows (e = 0) for the table tolerance check
+               W_rows={str(c): [float(v).hex() for v in r["W"][0, c]] for c in range(min(w.C, 4))})
+    return out
+
+
+def golden_bcd(iters: int) -> dict:
+    rows = []
+    k_prev = None
+    for it in range(iters):
+        w = make_workload("cfg5", iteration=it)
+        t0 = time.time()
+        S = oracle.S_exact(w, grouped=True)
+        W, _ = oracle.W_table(w, S)
+        if k_prev is None:
+            k_prev = oracle.bcd_init(w)
+            k0 = k_prev.tolist()
+        o = oracle.bcd_step(w, W[0], k_prev)
+        qv, qr = oracle.quantile(w)
+        rows.append(dict(iteration=it, checksum=w.checksum(), k_prev=k_prev.tolist(),
+                         k_next=o["k_next"].tolist(), W_star=[float(v).hex() for v in o["W_star"]],
+                         usage=[float(v).hex() for v in o["usage"]],
+                         feasible=o["feasible"].tolist(), q_value=qv.tolist(),
+                         seconds=round(time.time() - t0, 1)))
+        print(f"cfg5 iteration {it}: {rows[-1]['seconds']} s", flush=True)
+        k_prev = o["k_next"]
+    return dict(workload="cfg5", iterations=iters, k0=k0, rows=rows)
+
+
+def main(argv):
+    for arg in argv:
+        if arg.startswith("cfg5"):
+            iters = int(arg.split(":")[1]) if ":" in arg else 50
+            data = golden_bcd(iters)
+            path = os.path.join(HERE, "cfg5_bcd.json")
+        else:
+            data = golden_static(arg)
+            path = os.path.join(HERE, f"{arg}.json")
+        with open(path, "w") as f:
+            json.dump(data, f, indent=1)
+        print(f"wrote {path}", flush=True)
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])

@@ -1,0 +1,88 @@
+"""The fused block step on the GPU against the oracle's sweep (exact results)."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from workloads import make_workload, random_workload
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.fixture(scope="module")
+def ctx(dev):
+    import paper_2607_16892_amd as dro
+    c = dro.Context(dev.index or 0)
+    yield c
+    c.close()
+
+
+def gpu_step(ctx, w, dev, k_prev=None):
+    import torch
+    import paper_2607_16892_amd as dro
+    print(f"[gpu] block step {w.name} C={w.C} K={w.K} M={w.M} G={w.groups.G}", flush=True)
+    prob = dro.Problem.from_workload(w, dev)
+    eps = torch.from_numpy(w.eps[: w.C].copy()).to(dev)
+    grp = dro.Groups.from_numpy(w.groups.cap, w.groups.conc, w.groups.kappa, dev)
+    if k_prev is None:
+        kp = dro.bcd_init_state(ctx, prob)
+    else:
+        kp = torch.from_numpy(np.asarray(k_prev, np.int32)).to(dev)
+    k0 = kp.cpu().numpy()
+    o = dro.bcd_block_step(ctx, prob, eps, grp, kp)
+    torch.cuda.synchronize()
+    flags = ctx.take_flags()
+    return k0, {k: v.cpu().numpy() for k, v in o.items()}, flags
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_block_step_matches_oracle(ctx, dev, seed):
+    w = random_workload(seed=900 + seed, C=4, N=(200, 31, 500, 77), L=600, K=33, M=19, E=1,
+                        with_groups=True, G=3)
+    k0, g, flags = gpu_step(ctx, w, dev)
+    assert flags == 0
+    assert np.array_equal(k0, oracle.bcd_init(w))
+    S = oracle.S_exact(w)
+    W, _ = oracle.W_table(w, S)
+    o = oracle.bcd_step(w, W[0], k0)
+    assert np.array_equal(g["k_next"], o["k_next"])
+    assert np.array_equal(g["W_star"].view(np.uint64), o["W_star"].view(np.uint64))
+    assert np.array_equal(g["usage"].view(np.uint64), o["usage"].view(np.uint64))
+    assert np.array_equal(g["feasible"], o["feasible"])
+    qv, _ = oracle.quantile(w)
+    assert np.array_equal(g["q_value"], qv)
+
+
+def test_block_step_from_given_state(ctx, dev):
+    w = random_workload(seed=950, C=3, N=(90, 60, 150), L=400, K=21, M=13, E=1, with_groups=True, G=2)
+    k_prev = np.array([20, 0, 7], np.int32)
+    _, g, flags = gpu_step(ctx, w, dev, k_prev)
+    S = oracle.S_exact(w)
+    W, _ = oracle.W_table(w, S)
+    o = oracle.bcd_step(w, W[0], k_prev)
+    assert flags == 0
+    assert np.array_equal(g["k_next"], o["k_next"])
+    assert np.array_equal(g["W_star"].view(np.uint64), o["W_star"].view(np.uint64))
+
+
+def test_cfg5_iterations_against_stored_oracle(ctx, dev):
+    path = os.path.join(HERE, "golden", "cfg5_bcd.json")
+    if not os.path.exists(path):
+        pytest.skip("no stored oracle results for the drifting block-step loop")
+    gold = json.load(open(path))
+    k_prev = None
+    for row in gold["rows"][:3]:
+        w = make_workload("cfg5", iteration=row["iteration"])
+        assert w.checksum() == row["checksum"]
+        k0, g, flags = gpu_step(ctx, w, dev, k_prev)
+        assert flags == 0
+        assert k0.tolist() == row["k_prev"]
+        assert g["k_next"].tolist() == row["k_next"]
+        assert [float(v).hex() for v in g["W_star"]] == row["W_star"]
+        assert [float(v).hex() for v in g["usage"]] == row["usage"]
+        assert g["feasible"].tolist() == row["feasible"]
+        assert g["q_value"].tolist() == row["q_value"]
+        k_prev = g["k_next"]
