@@ -1,0 +1,200 @@
+#!/usr/bin/env python3
+"""Throughput of the DRO reservation path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload cfg3]
+
+One step is one pass of the whole hot path over the resident samples of the
+workload: the critical-fractile quantile of every class (class_quantile),
+the dense worst-case sums and the minimum over the multiplier grid
+(dro_cost_eval), and the exact lowest-index optimum (dro_argmin_reservation).
+The default workload is 16 classes x 1e6 heavy-tailed synthetic lengths,
+K = 2048 reservation levels, M = 256 multipliers.  The fused block step is
+timed separately on the drifting 8-class x 4e6 workload (6 serving groups).
+
+Prints ONE JSON line.  `value` is evaluations per second of the whole step
+(one evaluation = one (class, reservation, multiplier, sample) term).
+`roofline` prices the dense kernel's algorithmic fp32 work (7 operations per
+evaluation: two multiply-adds, a 3-way max, an accumulate) against the fp32
+vector peak; `cpu_baseline` times the CPU oracle's dense fp64 evaluation on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_PEAK_TFLOPS = 157.3          # MI355X fp32 vector: 256 CU x 64 lanes x 2 (FMA) x 2 (packed) x 2.4 GHz
+FLOPS_PER_EVAL = 7                # 2 FMA (4) + 3-way max (2) + accumulate (1)
+METRIC = "DRO cost evals/sec (class×r×λ×sample per s) + % fp32 VALU peak"
+
+
+def _log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, n_samples: int):
+    """Oracle dense fp64 on the first n samples of class 0, every grid point and multiplier."""
+    import numpy as np
+    import oracle
+    from workloads.configs import Workload
+    xs = w.samples_of(0)[:n_samples].copy()
+    sub = Workload("sample", 1, np.array([0, len(xs)], np.int64), None, xs, w.L[:1].copy(), w.eta,
+                   w.lam, w.c_p[:1].copy(), w.c_w[:1].copy(), 1, w.eps[:1].copy())
+    t = time.perf_counter()
+    oracle.S_f64(sub)
+    dt = time.perf_counter() - t
+    return dict(value=sub.evals / dt, unit="evals/s", cores=oracle.threads(), kind="oracle",
+                sample=f"class 0 of {w.name}, first {len(xs)} samples x K={w.K} x M={w.M} "
+                       f"({sub.evals:.3g} evaluations, dense fp64, {dt:.1f} s)")
+
+
+def bench_bcd(ctx, dev, iters: int):
+    """Fused block step on the drifting workload: ms per iteration (inputs resident)."""
+    import torch
+    import numpy as np
+    import paper_2607_16892_amd as dro
+    from workloads import make_workload
+    w = make_workload("cfg5", iteration=0)
+    prob = dro.Problem.from_workload(w, dev)
+    grp = dro.Groups.from_numpy(w.groups.cap, w.groups.conc, w.groups.kappa, dev)
+    k = dro.bcd_init_state(ctx, prob)
+    times = []
+    binding = 0
+    for it in range(iters):
+        if it:
+            w = make_workload("cfg5", iteration=it)
+            prob.replace_samples(w.offsets, w.xi)
+        eps = torch.from_numpy(w.eps.copy()).to(dev)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        o = dro.bcd_block_step(ctx, prob, eps, grp, k)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+        k = o["k_next"]
+        usage = o["usage"].cpu().numpy()
+        binding = int((usage > 0.98 * w.groups.cap).sum())
+    flags = ctx.take_flags()
+    ms = float(np.median(times)) if times else None
+    return dict(workload="cfg5: 8 classes x 4e6 drifting lognormal, K=2048, M=256, G=6",
+                iters=iters, ms_per_iter=ms, evals_per_iter=w.evals,
+                evals_per_s=(w.evals / (ms / 1e3)) if ms else None,
+                binding_groups_last_iter=binding, flags=flags)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="cfg3")
+    ap.add_argument("--cpu-samples", type=int, default=8192)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--bcd-iters", type=int, default=3)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the work shards over classes with no exchange; see DESIGN.md). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2607_16892_amd as dro
+    from workloads import make_workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    _log(f"generating {args.workload}")
+    w = make_workload(args.workload)
+    ctx = dro.Context(0)
+    prob = dro.Problem.from_workload(w, dev)
+    eps = torch.from_numpy(w.eps.copy()).to(dev)
+    dro.dro_validate(ctx, prob, eps)
+    E = w.E
+    S = torch.empty((w.C, w.K, w.M), dtype=torch.float64, device=dev)
+    W = torch.empty((E, w.C, w.K), dtype=torch.float64, device=dev)
+    m_star = torch.empty((E, w.C, w.K), dtype=torch.int32, device=dev)
+    outs = {}
+
+    def step(ev_pair=None):
+        dro.class_quantile(ctx, prob)
+        if ev_pair:
+            ev_pair[0].record()
+        dro.dro_cost_eval(ctx, prob, eps, W=W, m_star=m_star, S=S)
+        if ev_pair:
+            ev_pair[1].record()
+        outs.update(dro.dro_argmin_reservation(ctx, prob, eps, S))
+
+    _log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(args.steps)]
+    _log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(pairs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    flags = ctx.take_flags()
+    ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
+    dense_ms = float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+    evals = w.evals
+    value = evals / (ms_step / 1e3)
+    achieved = evals * FLOPS_PER_EVAL / (dense_ms / 1e3) / 1e12
+    _log(f"step {ms_step:.2f} ms, dense {dense_ms:.2f} ms, {value:.3e} evals/s, flags={flags}")
+
+    bcd = None
+    if args.bcd_iters > 0:
+        _log(f"block step, {args.bcd_iters} iterations")
+        bcd = bench_bcd(ctx, dev, args.bcd_iters)
+    cpu = None
+    if not args.no_cpu_baseline:
+        _log("cpu baseline (oracle)")
+        cpu = cpu_baseline(w, args.cpu_samples)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.meta.get('desc', '')}", "C": w.C, "N_per_class": w.n_of(0),
+                   "K": w.K, "M": w.M, "E": E, "evals_per_step": evals},
+        "pct_fp32_valu_peak": 100.0 * achieved / FP32_PEAK_TFLOPS,
+        "roofline": {"bound": "alu", "kernel": "dense_kernel (dro_cost_eval)",
+                     "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / FP32_PEAK_TFLOPS, "traffic": None,
+                     "launch_ms": dense_ms, "flops_per_eval": FLOPS_PER_EVAL,
+                     "evals_per_launch": evals},
+        "cpu_baseline": cpu,
+        "block_step": bcd,
+        "flags": flags,
+    }
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()
