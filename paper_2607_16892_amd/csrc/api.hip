@@ -13,6 +13,7 @@
 struct dro_ctx {
     int device = 0;
     int num_cu = 256;
+    int dense_bpc = 1;  // resident dense blocks per compute unit
     void *ws = nullptr;
     size_t ws_size = 0;
     uint32_t *flags = nullptr;  // device word of DRO_FLAG_* bits
@@ -131,7 +132,10 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
     return DRO_OK;
 }
 
-DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu)
+// Tiles of kTK x kTM pairs per lane; samples of a class split into P slices so
+// that the grid fills whole rounds of resident blocks (cap = CUs x blocks/CU):
+// the smallest P whose last round is at least 97 % full, slices >= 1024 samples.
+DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
 {
     DensePlan pl{};
     const int need_m = (M + kTM - 1) / kTM;
@@ -141,12 +145,22 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu)
     pl.tiles_k = (K + kTK * pl.lanes_k - 1) / (kTK * pl.lanes_k);
     pl.tiles_m = (M + kTM * pl.lanes_m - 1) / (kTM * pl.lanes_m);
     const long long base = (long long)C * pl.tiles_k * pl.tiles_m;
-    const long long target = 4LL * num_cu;
-    long long P = (target + base - 1) / base;
-    P = std::min(P, std::max(1LL, max_n / 128));
-    P = std::max(P, 1LL);
-    pl.P = (int)P;
-    pl.blocks = base * P;
+    const long long cap = (long long)num_cu * std::max(bpc, 1);
+    const long long maxP = std::max(1LL, std::min(64LL, max_n / 1024));
+    long long bestP = 1;
+    double best = -1.0;
+    for (long long P = 1; P <= maxP; ++P) {
+        const long long n = base * P;
+        const long long rounds = (n + cap - 1) / cap;
+        const double fill = (double)n / (double)(rounds * cap);
+        if (fill > best + 1e-9) {
+            best = fill;
+            bestP = P;
+        }
+        if (fill >= 0.97) break;
+    }
+    pl.P = (int)bestP;
+    pl.blocks = base * bestP;
     return pl;
 }
 
@@ -325,6 +339,7 @@ int dro_create(int hip_device, dro_ctx **out)
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, hip_device) == hipSuccess && prop.multiProcessorCount > 0)
         ctx->num_cu = prop.multiProcessorCount;
+    ctx->dense_bpc = dense_blocks_per_cu();
     if (hipMalloc(&ctx->flags, sizeof(uint32_t)) != hipSuccess ||
         hipMemset(ctx->flags, 0, sizeof(uint32_t)) != hipSuccess) {
         delete ctx;
@@ -443,7 +458,7 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     DeviceGuard g(ctx->device);
     if (!g.ok) return fail(ctx, DRO_EHIP, "cannot select device %d", ctx->device);
     hipStream_t st = (hipStream_t)stream;
-    const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu);
+    const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     rc = ensure_ws(ctx, dense_bytes(p, pl, S == nullptr), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
@@ -518,7 +533,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     DeviceGuard g(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
-    const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu);
+    const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const int P = refine_slices(sh.max_n);
     const size_t need = dense_bytes(p, pl, true) + rup((size_t)p->S * kHistBins * 4) +
                         refine_bytes(C, P) + rup((size_t)C * 8) + 3 * rup((size_t)C * 4);

@@ -6,30 +6,59 @@
 // C * K * M * N_c terms in all.  This is max-plus arithmetic, not a dense
 // contraction, so it runs on the fp32 VALU: every lane keeps a kTK x kTM
 // register tile of (grid point, multiplier) accumulators and streams the
-// samples of its class from LDS, where each tile of kTileN samples is
-// staged once per block and read back as a wave-wide broadcast.
+// samples of its class from LDS, where each tile of kTileN samples is staged
+// once per block and read back as a wave-wide broadcast.
 //
-// Per sample x and grid point eta the lambda-independent parts are formed
-// once and shared by the kTM multipliers of the lane:
-//   A_p = c_p (x - eta),  A_w = c_w (eta - x),  A = max(A_p, A_w) = Q(eta, x)
-// and per multiplier lam the two boundary candidates are
-//   c_w eta - lam x           = A_w + (c_w - lam) x
-//   c_p (L - eta) - lam (L-x) = A_p + (c_p - lam) (L - x)
-// so that every rounded constant multiplies a quantity no larger than the
-// candidate it feeds (the large constants c_w eta and c_p (L - eta) are never
-// rounded on their own).  phi = max3(A, both candidates).
+// Form of the term.  With B = c_w eta, C = c_p (L - eta), a1 = min(g, c_w) and
+// a2 = min(g, c_p), the three candidates of Step 4 reduce, for 0 <= x, eta <= L,
+// to the maximum of two lines (Q(eta, x) itself is the larger of c_w(eta - x)
+// and c_p(x - eta), and for x, L - x >= 0 the smaller slope wins each pair):
+//     phi = max(y1, y2),  y1 = B - a1 x,  y2 = C - a2 (L - x),
+// which cross at x0 = (B - C + a2 L) / (a1 + a2).  Hence, exactly,
+//     phi = y1 + (a1 + a2) relu(x - x0)      (used when c_w <= c_p)
+//     phi = y2 + (a1 + a2) relu(x0 - x)      (used when c_w >  c_p)
+// The line sums need only N and sum(x) of the slice and are formed in fp64;
+// every (c, k, m, n) term still contributes its relu, evaluated per sample.
+// The relu is one instruction: samples are staged as +-x * 2^-16 and the
+// lane adds -+x0 * 2^-16 with the [0, 1] output clamp, exact while |x - x0| <
+// 2^16 (x0 is clamped to [-1, L + 1], where relu is linear in the samples, and
+// the clamped part is added back in the epilogue).  Choosing the side of the
+// steeper line keeps the relu sum below twice the class's share of S, so the
+// fp32 accumulation carries no cancellation.  Per evaluation the inner loop is
+//     v_add_f32 t, xs, a clamp ;  v_add_f32 acc, acc, t
+// two fp32 VALU instructions that gfx950 issues at the double rate.
 //
-// Accuracy: fp32 runs of at most kRun samples are folded into fp64 in a fixed
-// order, so the result is deterministic for a given launch plan.
+// Accuracy: fp32 runs of kRun samples folded into fp64 in a fixed order, so
+// the result is deterministic for a given launch plan.
 #include "dro_internal.h"
 
 namespace dro {
 
 __device__ __forceinline__ int seg_of(const int32_t *seg, int c) { return seg ? seg[c] : c; }
 
+// Crossing point of the two lines and the epilogue constants of one pair.
+struct PairLines {
+    double B, C, a1, a2, x0, x0c;
+};
+
+__device__ __forceinline__ PairLines pair_lines(float cp, float cw, float lam, int eta, int L)
+{
+    PairLines r;
+    const float a1 = lam < cw ? lam : cw;
+    const float a2 = lam < cp ? lam : cp;
+    r.a1 = a1;
+    r.a2 = a2;
+    r.B = (double)cw * (double)eta;
+    r.C = (double)cp * (double)(L - eta);
+    r.x0 = (r.B - r.C + (double)a2 * (double)L) / ((double)a1 + (double)a2);
+    r.x0c = r.x0 < -1.0 ? -1.0 : (r.x0 > (double)L + 1.0 ? (double)L + 1.0 : r.x0);
+    return r;
+}
+
 __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
 {
     __shared__ __attribute__((aligned(16))) float xs[kTileN];
+    __shared__ long long red[kThreads];
 
     const DensePlan pl = a.plan;
     long long b = blockIdx.x;
@@ -52,21 +81,26 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
     const long long hi = n_beg + (N * (p + 1)) / pl.P;
 
     const float cp = a.c_p[c], cw = a.c_w[c];
-    const float Lf = (float)a.L[c];
+    const int L = a.L[c];
+    const bool upper = cw <= cp;                          // relu on x > x0
+    const float xscale = upper ? 0x1p-16f : -0x1p-16f;    // staged sample sign and scale
 
     int kk[kTK], mm[kTM];
-    float etaf[kTK], gw[kTM], gp[kTM];
+#pragma unroll
+    for (int i = 0; i < kTK; ++i) kk[i] = tk * BK + lk + i * pl.lanes_k;
+#pragma unroll
+    for (int j = 0; j < kTM; ++j) mm[j] = tm * BM + lm + j * pl.lanes_m;
+
+    float add[kTK][kTM];
 #pragma unroll
     for (int i = 0; i < kTK; ++i) {
-        kk[i] = tk * BK + lk + i * pl.lanes_k;
-        etaf[i] = (float)a.eta[min(kk[i], a.K - 1)];
-    }
+        const int eta = a.eta[min(kk[i], a.K - 1)];
 #pragma unroll
-    for (int j = 0; j < kTM; ++j) {
-        mm[j] = tm * BM + lm + j * pl.lanes_m;
-        const float lam = a.lam[min(mm[j], a.M - 1)];
-        gw[j] = cw - lam;
-        gp[j] = cp - lam;
+        for (int j = 0; j < kTM; ++j) {
+            const PairLines q = pair_lines(cp, cw, a.lam[min(mm[j], a.M - 1)], eta, L);
+            const float x0f = (float)q.x0c;
+            add[i][j] = upper ? -(x0f * 0x1p-16f) : x0f * 0x1p-16f;
+        }
     }
 
     double acc64[kTK][kTM];
@@ -75,10 +109,15 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
 #pragma unroll
         for (int j = 0; j < kTM; ++j) acc64[i][j] = 0.0;
 
+    long long xsum = 0;  // this thread's share of the slice's sample sum
     for (long long base = lo; base < hi; base += kTileN) {
         const int len = (int)min((long long)kTileN, hi - base);
         __syncthreads();
-        for (int i = t; i < len; i += kThreads) xs[i] = (float)a.xi[base + i];
+        for (int i = t; i < len; i += kThreads) {
+            const int x = a.xi[base + i];
+            xsum += x;
+            xs[i] = (float)x * xscale;
+        }
         __syncthreads();
 
         for (int u0 = 0; u0 < len; u0 += kRun) {
@@ -90,20 +129,11 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
                 for (int j = 0; j < kTM; ++j) acc[i][j] = 0.0f;
 
             auto step = [&](float x) {
-                const float lx = Lf - x;
 #pragma unroll
-                for (int i = 0; i < kTK; ++i) {
-                    const float d = x - etaf[i];
-                    const float Ap = cp * d;
-                    const float Aw = -(cw * d);
-                    const float A = fmaxf(Ap, Aw);
+                for (int i = 0; i < kTK; ++i)
 #pragma unroll
-                    for (int j = 0; j < kTM; ++j) {
-                        const float t0 = fmaf(gw[j], x, Aw);
-                        const float tL = fmaf(gp[j], lx, Ap);
-                        acc[i][j] += fmaxf(fmaxf(A, t0), tL);
-                    }
-                }
+                    for (int j = 0; j < kTM; ++j)
+                        acc[i][j] += __builtin_amdgcn_fmed3f(x + add[i][j], 0.0f, 1.0f);
             };
 
             int u = 0;
@@ -123,16 +153,45 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
         }
     }
 
+    // slice sample sum (exact integer), shared by every pair of the block
+    red[t] = xsum;
+    __syncthreads();
+    for (int w = kThreads / 2; w > 0; w >>= 1) {
+        if (t < w) red[t] += red[t + w];
+        __syncthreads();
+    }
+    const double sx = (double)red[0];
+    const double n = (double)(hi - lo);
+
     double *out = a.out + ((long long)p * a.C + c) * (long long)a.K * a.M;
 #pragma unroll
     for (int i = 0; i < kTK; ++i) {
         if (kk[i] >= a.K) continue;
+        const int eta = a.eta[kk[i]];
 #pragma unroll
         for (int j = 0; j < kTM; ++j) {
             if (mm[j] >= a.M) continue;
-            out[(long long)kk[i] * a.M + mm[j]] = acc64[i][j];
+            const PairLines q = pair_lines(cp, cw, a.lam[mm[j]], eta, L);
+            const double relu = acc64[i][j] * 65536.0;
+            double line, corr = 0.0;
+            if (upper) {
+                line = n * q.B - q.a1 * sx;
+                if (q.x0 < q.x0c) corr = n * (q.x0c - q.x0);
+            } else {
+                line = n * (q.C - q.a2 * (double)L) + q.a2 * sx;
+                if (q.x0 > q.x0c) corr = n * (q.x0 - q.x0c);
+            }
+            out[(long long)kk[i] * a.M + mm[j]] = line + (q.a1 + q.a2) * (relu + corr);
         }
     }
+}
+
+int dense_blocks_per_cu()
+{
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dense_kernel, kThreads, 0) != hipSuccess || n < 1)
+        n = 1;
+    return n;
 }
 
 hipError_t launch_dense(const DenseArgs &a, hipStream_t st)

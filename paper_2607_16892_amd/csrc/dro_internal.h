@@ -41,6 +41,8 @@ struct DenseArgs {
 };
 
 hipError_t launch_dense(const DenseArgs &a, hipStream_t st);
+// resident dense blocks per compute unit (occupancy of dense_kernel)
+int dense_blocks_per_cu();
 // S[i] = sum_p part[p * n + i], p ascending
 hipError_t launch_reduce_slices(const double *part, int P, long long n, double *S, hipStream_t st);
 // W[e,c,k] = min_m RN(RN(lam_m eps[e,c]) + RN(S[c,k,m] / N_c)), lowest m

@@ -64,7 +64,9 @@ def check_against_oracle(w, g, kmax=None):
     assert np.array_equal(g["q_value"], ref["q_value"])
     assert np.array_equal(g["q_rank"], ref["q_rank"])
     assert g["flags"] == 0
-    print(f"  S rel err {np.max(errS / np.maximum(Sx, 1e-300)):.2e}  "
+    relS = errS / np.maximum(Sx, 1e-300)
+    worst = np.unravel_index(np.argmax(relS), relS.shape)
+    print(f"  S rel err {relS.max():.2e} at (c,k,m)={tuple(int(v) for v in worst)}  "
           f"W rel err {np.max(errW / np.maximum(ref['W'], 1e-300)):.2e}", flush=True)
 
 
