@@ -140,7 +140,7 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     DensePlan pl{};
     const int need_m = (M + kTM - 1) / kTM;
     pl.lanes_m = 1;
-    while (pl.lanes_m < need_m && pl.lanes_m < 16) pl.lanes_m *= 2;
+    while (pl.lanes_m < need_m && pl.lanes_m < kThreads) pl.lanes_m *= 2;
     pl.lanes_k = kThreads / pl.lanes_m;
     pl.tiles_k = (K + kTK * pl.lanes_k - 1) / (kTK * pl.lanes_k);
     pl.tiles_m = (M + kTM * pl.lanes_m - 1) / (kTM * pl.lanes_m);

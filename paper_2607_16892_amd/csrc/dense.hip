@@ -19,14 +19,19 @@
 //     phi = y2 + (a1 + a2) relu(x0 - x)      (used when c_w >  c_p)
 // The line sums need only N and sum(x) of the slice and are formed in fp64;
 // every (c, k, m, n) term still contributes its relu, evaluated per sample.
-// The relu is one instruction: samples are staged as +-x * 2^-16 and the
-// lane adds -+x0 * 2^-16 with the [0, 1] output clamp, exact while |x - x0| <
-// 2^16 (x0 is clamped to [-1, L + 1], where relu is linear in the samples, and
-// the clamped part is added back in the epilogue).  Choosing the side of the
-// steeper line keeps the relu sum below twice the class's share of S, so the
-// fp32 accumulation carries no cancellation.  Per evaluation the inner loop is
-//     v_add_f32 t, xs, a clamp ;  v_add_f32 acc, acc, t
-// two fp32 VALU instructions that gfx950 issues at the double rate.
+// The kink is measured from the grid point, x - x0 = (x - eta) - d with
+// d = x0 - eta: x - eta is an exact integer formed once per (k, sample) and
+// shared by the lane's kTM multipliers, and d is rounded to fp32 relative to
+// its own size (it is 0, hence exact, for every lam >= max(c_p, c_w)).  The
+// relu is then one instruction: u = +-(x - eta) 2^-16 plus -+d 2^-16 with the
+// [0, 1] output clamp, exact while |x - x0| < 2^16 (x0 is clamped to
+// [-1, L + 1], where relu is linear in the samples, and the clamped part is
+// added back in the epilogue).  Choosing the side of the steeper line keeps
+// the relu sum below twice the class's share of S, so the fp32 accumulation
+// carries no cancellation.  Per evaluation the inner loop is
+//     v_add_f32 t, u, a clamp ;  v_add_f32 acc, acc, t
+// two fp32 VALU instructions that gfx950 issues at the double rate, plus one
+// v_fma_f32 per (k, sample) shared by kTM evaluations.
 //
 // Accuracy: fp32 runs of kRun samples folded into fp64 in a fixed order, so
 // the result is deterministic for a given launch plan.
@@ -83,23 +88,22 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
     const float cp = a.c_p[c], cw = a.c_w[c];
     const int L = a.L[c];
     const bool upper = cw <= cp;                          // relu on x > x0
-    const float xscale = upper ? 0x1p-16f : -0x1p-16f;    // staged sample sign and scale
+    const float sc = upper ? 0x1p-16f : -0x1p-16f;        // sign and scale of x - eta
 
-    int kk[kTK], mm[kTM];
-#pragma unroll
-    for (int i = 0; i < kTK; ++i) kk[i] = tk * BK + lk + i * pl.lanes_k;
-#pragma unroll
-    for (int j = 0; j < kTM; ++j) mm[j] = tm * BM + lm + j * pl.lanes_m;
+    // grid point k_i = k0 + i * lanes_k, multiplier m_j = m0 + j * lanes_m
+    // (recomputed where needed rather than held in registers)
+    const int k0 = tk * BK + lk, m0 = tm * BM + lm;
 
-    float add[kTK][kTM];
+    float eoff[kTK];        // -+eta 2^-16
+    float add[kTK][kTM];    // -+(x0 - eta) 2^-16
 #pragma unroll
     for (int i = 0; i < kTK; ++i) {
-        const int eta = a.eta[min(kk[i], a.K - 1)];
+        const int eta = a.eta[min(k0 + i * pl.lanes_k, a.K - 1)];
+        eoff[i] = -(float)eta * sc;
 #pragma unroll
         for (int j = 0; j < kTM; ++j) {
-            const PairLines q = pair_lines(cp, cw, a.lam[min(mm[j], a.M - 1)], eta, L);
-            const float x0f = (float)q.x0c;
-            add[i][j] = upper ? -(x0f * 0x1p-16f) : x0f * 0x1p-16f;
+            const PairLines q = pair_lines(cp, cw, a.lam[min(m0 + j * pl.lanes_m, a.M - 1)], eta, L);
+            add[i][j] = -(float)(q.x0c - (double)eta) * sc;
         }
     }
 
@@ -116,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
         for (int i = t; i < len; i += kThreads) {
             const int x = a.xi[base + i];
             xsum += x;
-            xs[i] = (float)x * xscale;
+            xs[i] = (float)x;
         }
         __syncthreads();
 
@@ -130,10 +134,12 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
 
             auto step = [&](float x) {
 #pragma unroll
-                for (int i = 0; i < kTK; ++i)
+                for (int i = 0; i < kTK; ++i) {
+                    const float u = fmaf(x, sc, eoff[i]);  // +-(x - eta) 2^-16, exact
 #pragma unroll
                     for (int j = 0; j < kTM; ++j)
-                        acc[i][j] += __builtin_amdgcn_fmed3f(x + add[i][j], 0.0f, 1.0f);
+                        acc[i][j] += __builtin_amdgcn_fmed3f(u + add[i][j], 0.0f, 1.0f);
+                }
             };
 
             int u = 0;
@@ -163,15 +169,22 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
     const double sx = (double)red[0];
     const double n = (double)(hi - lo);
 
+    // The epilogue recomputes the pair constants; hiding the indices from the
+    // optimiser keeps it from holding the set-up values live across the loop.
+    int k0e = k0, m0e = m0;
+    asm volatile("" : "+v"(k0e), "+v"(m0e));
+
     double *out = a.out + ((long long)p * a.C + c) * (long long)a.K * a.M;
 #pragma unroll
     for (int i = 0; i < kTK; ++i) {
-        if (kk[i] >= a.K) continue;
-        const int eta = a.eta[kk[i]];
+        const int k = k0e + i * pl.lanes_k;
+        if (k >= a.K) continue;
+        const int eta = a.eta[k];
 #pragma unroll
         for (int j = 0; j < kTM; ++j) {
-            if (mm[j] >= a.M) continue;
-            const PairLines q = pair_lines(cp, cw, a.lam[mm[j]], eta, L);
+            const int m = m0e + j * pl.lanes_m;
+            if (m >= a.M) continue;
+            const PairLines q = pair_lines(cp, cw, a.lam[m], eta, L);
             const double relu = acc64[i][j] * 65536.0;
             double line, corr = 0.0;
             if (upper) {
@@ -181,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
                 line = n * (q.C - q.a2 * (double)L) + q.a2 * sx;
                 if (q.x0 > q.x0c) corr = n * (q.x0 - q.x0c);
             }
-            out[(long long)kk[i] * a.M + mm[j]] = line + (q.a1 + q.a2) * (relu + corr);
+            out[(long long)k * a.M + m] = line + (q.a1 + q.a2) * (relu + corr);
         }
     }
 }

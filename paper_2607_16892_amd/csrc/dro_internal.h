@@ -10,12 +10,12 @@
 namespace dro {
 
 // ---- dense evaluation -------------------------------------------------------
-// Every lane owns a register tile of TK grid points x TM multipliers; a
+// Every lane owns a register tile of kTK grid points x kTM multipliers; a
 // 256-lane block covers (TK * lanes_k) x (TM * lanes_m) pairs of one class and
 // one slice of that class's samples, staged through LDS.
 constexpr int kThreads = 256;
-constexpr int kTK = 4;
-constexpr int kTM = 8;
+constexpr int kTK = 1;
+constexpr int kTM = 32;
 constexpr int kTileN = 1024;  // samples staged per LDS tile
 constexpr int kRun = 64;      // fp32 run length before the fp64 fold
 

@@ -143,3 +143,27 @@ def test_large_config_against_stored_oracle(ctx, dev, name):
         ref = oracle._load().oracle_fix_to_double(int(ex.hi[i]), int(ex.lo[i]))
         got = g["S"][cs[i], ks[i], ms[i]]
         assert abs(got - ref) <= REL * ref, (cs[i], ks[i], ms[i], got, ref)
+
+
+def _kink_workload():
+    """Every sample sits just above the crossing point x0 of the two lines of phi.
+
+    With c_w = c_p = 1.00055 lam_37 and eta = 30000 the crossing point is
+    x0 = 30007.49 while phi there is only about 6.5.  A kink rounded to fp32 in
+    absolute terms (error up to 2^-10 tokens at this size) would move S by
+    about 2e-4 relative; measured from eta it is exact to ~1e-7.
+    """
+    from workloads import eta_grid, lam_grid
+    from workloads.configs import Workload
+    L, K, M = 32768, 2049, 64
+    lam = lam_grid(M)
+    c = np.float32(lam[37] * np.float32(1.00055))
+    xs = np.full(2000, 30008, np.int32)
+    return Workload("kink", 1, np.array([0, xs.size], np.int64), None, xs,
+                    np.array([L], np.int32), eta_grid(K, L), lam, np.array([c], np.float32),
+                    np.array([c], np.float32), 2, np.array([0.0, 40.0], np.float32))
+
+
+def test_samples_on_the_kink(ctx, dev):
+    w = _kink_workload()
+    check_against_oracle(w, run_gpu(ctx, w, dev))
