@@ -164,7 +164,7 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     return pl;
 }
 
-int refine_slices(long long max_n) { return (int)std::min(32LL, std::max(1LL, max_n / 16384)); }
+int refine_slices(long long max_n) { return (int)std::min(256LL, std::max(1LL, max_n / 8192)); }
 
 // S (approximate) into `S`, using `part` when the plan splits samples.
 int run_dense(dro_ctx *ctx, const dro_problem *p, const Shape &sh, double *S, double *part,
@@ -201,22 +201,25 @@ size_t dense_bytes(const dro_problem *p, const DensePlan &pl, bool need_S)
 
 struct RefineBufs {
     int32_t *cand, *count;
-    double *thresh;
+    double *thresh, *chunk_min;
     uint64_t *part;
 };
 
-size_t refine_bytes(int EC, int P)
+size_t band_chunks(int K) { return (size_t)(K + kBandKC - 1) / kBandKC; }
+
+size_t refine_bytes(int EC, int P, int K)
 {
     return rup((size_t)EC * kBandCap * 4) + rup((size_t)EC * 4) + rup((size_t)EC * 8) +
-           rup((size_t)EC * kBandCap * P * 16);
+           rup((size_t)EC * band_chunks(K) * 8) + rup((size_t)EC * kBandCap * P * 16);
 }
 
-RefineBufs take_refine(Arena &ar, int EC, int P)
+RefineBufs take_refine(Arena &ar, int EC, int P, int K)
 {
     RefineBufs r;
     r.cand = ar.take<int32_t>((size_t)EC * kBandCap);
     r.count = ar.take<int32_t>(EC);
     r.thresh = ar.take<double>(EC);
+    r.chunk_min = ar.take<double>((size_t)EC * band_chunks(K));
     r.part = ar.take<uint64_t>((size_t)EC * kBandCap * P * 2);
     return r;
 }
@@ -247,7 +250,7 @@ int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, cons
     b.count = rb.count;
     b.thresh = rb.thresh;
     b.flags = ctx->flags;
-    HIPCHK(launch_band(b, st));
+    HIPCHK(launch_band(b, rb.chunk_min, st));
 
     RefineArgs r{};
     r.offsets = p->offsets;
@@ -485,10 +488,10 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     hipStream_t st = (hipStream_t)stream;
     const int EC = E * p->C;
     const int P = refine_slices(sh.max_n);
-    rc = ensure_ws(ctx, refine_bytes(EC, P), st);
+    rc = ensure_ws(ctx, refine_bytes(EC, P, p->K), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
-    RefineBufs rb = take_refine(ar, EC, P);
+    RefineBufs rb = take_refine(ar, EC, P, p->K);
     return run_argmin(ctx, p, E, eps, S, k_max, 0, -1, rb, P, k_star, W_star, m_at_star, st);
 }
 
@@ -515,7 +518,12 @@ int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t
     if (rc) return rc;
     if (!k0) return fail(ctx, DRO_EINVAL, "k0 must be non-NULL");
     DeviceGuard g(ctx->device);
-    HIPCHK(launch_bcd_init(p->offsets, p->seg, p->xi, p->eta, p->C, p->K, k0, (hipStream_t)stream));
+    hipStream_t st = (hipStream_t)stream;
+    rc = ensure_ws(ctx, rup((size_t)p->C * 8), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    unsigned long long *sums = ar.take<unsigned long long>(p->C);
+    HIPCHK(launch_bcd_init(p->offsets, p->seg, p->xi, p->eta, p->C, p->K, sh.max_n, sums, k0, st));
     return DRO_OK;
 }
 
@@ -536,7 +544,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const int P = refine_slices(sh.max_n);
     const size_t need = dense_bytes(p, pl, true) + rup((size_t)p->S * kHistBins * 4) +
-                        refine_bytes(C, P) + rup((size_t)C * 8) + 3 * rup((size_t)C * 4);
+                        refine_bytes(C, P, p->K) + rup((size_t)C * 8) + 3 * rup((size_t)C * 4);
     rc = ensure_ws(ctx, need, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
@@ -544,7 +552,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     double *S = ar.take<double>(ckm);
     double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
     uint32_t *hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
-    RefineBufs rb = take_refine(ar, C, P);
+    RefineBufs rb = take_refine(ar, C, P, p->K);
     int64_t *q_rank = ar.take<int64_t>(C);
     int32_t *kmax = ar.take<int32_t>(C);
     int32_t *kcur = ar.take<int32_t>(C);

@@ -53,6 +53,7 @@ hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const
 // ---- exact screening / refine ----------------------------------------------
 constexpr int kBandCap = 256;     // candidates kept per (e, c)
 constexpr double kBandTau = 1e-4; // relative width of the screening band
+constexpr int kBandKC = 16;       // grid points per screening block
 
 struct BandArgs {
     const double *S;  // approximate [C][K][M]
@@ -67,11 +68,12 @@ struct BandArgs {
     int E, C, K, M;
     int e_row, c_only;    // c_only >= 0: one (e_row, c_only) problem only
     int32_t *cand;        // [EC][kBandCap] packed k * M + m
-    int32_t *count;       // [EC]
+    int32_t *count;       // [EC] (raw count; may exceed kBandCap)
     double *thresh;       // [EC]
     uint32_t *flags;
 };
-hipError_t launch_band(const BandArgs &a, hipStream_t st);
+// chunk_min: [EC][ceil(K / kBandKC)] scratch
+hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st);
 
 struct RefineArgs {
     const int64_t *offsets;
@@ -119,8 +121,10 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
                          int64_t *q_rank, hipStream_t st);
 
 // ---- block step ----------------------------------------------------------------
+// sums: [C] scratch
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
-                           const int32_t *eta, int C, int K, int32_t *k0, hipStream_t st);
+                           const int32_t *eta, int C, int K, long long max_n,
+                           unsigned long long *sums, int32_t *k0, hipStream_t st);
 hipError_t launch_bcd_kmax(const int32_t *eta, int C, int K, int G, const float *cap,
                            const float *conc, float kappa, const int32_t *kcur, int c,
                            int32_t *kmax, uint8_t *feasible, hipStream_t st);

@@ -10,6 +10,8 @@
 // 64-bit integers and summed exactly in 128-bit integers.  The reported value
 // is J = RN(RN(lam eps) + RN(RN(S) / N)) with RN(S) the correctly rounded
 // double of the exact sum.
+#include <algorithm>
+
 #include "dro_internal.h"
 
 namespace dro {
@@ -62,85 +64,129 @@ __device__ __forceinline__ void add128(uint64_t &lo, uint64_t &hi, uint64_t blo,
     lo = r;
 }
 
-// ------------------------------------------------------------------ band ----
-// Block per (e, c).  Screens every (k <= kmax, m) by the approximate dual value
-// and keeps those within a relative band of the approximate minimum.  For
-// lam_m >= max(c_p, c_w) every sample keeps its own point, so S is the SAA sum
-// for all such m and J can only grow with m: only the first of them can be a
-// lowest-index minimiser, and the others are not screened.
-__global__ __launch_bounds__(256) void band_kernel(BandArgs a)
+__global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
 {
-    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
-    const int e = ec / a.C, c = ec % a.C;
-    const int t = threadIdx.x;
-    const int s = seg_of_x(a.seg, c);
-    const double N = (double)(a.offsets[s + 1] - a.offsets[s]);
-    const float cp = a.c_p[c], cw = a.c_w[c];
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// ------------------------------------------------------------------ band ----
+// Screening, over (problem ec = e*C + c, chunk of kBandKC grid points):
+//   band_min:     the smallest approximate dual value J~ = lam eps + S~ / N of
+//                 the chunk's pairs (k <= kmax, m <= m_first);
+//   band_collect: threshold T = (1 + tau) min J~ + slack from the chunk minima,
+//                 then every pair with J~ <= T appended to the problem's list
+//                 through a global counter.  The list order is irrelevant: the
+//                 refine evaluates every listed pair exactly and keeps the
+//                 lowest (J, k, m).
+// For lam_m >= max(c_p, c_w) every sample keeps its own point, so S is the SAA
+// sum for all such m and J can only grow with m: only the first of them
+// (m_first) can be a lowest-index minimiser, and the others are not screened.
+struct BandProblem {
+    int ec, c, kmax, mlim;
+    double ninv, ev, slack;
+};
+
+__device__ BandProblem band_problem(const BandArgs &a, int ec)
+{
+    __shared__ int s_mf;
+    BandProblem q;
+    q.ec = ec;
+    q.c = ec % a.C;
+    const int e = ec / a.C;
+    const float cp = a.c_p[q.c], cw = a.c_w[q.c];
     const float top = cp > cw ? cp : cw;
-
-    __shared__ int s_mfirst;
-    __shared__ double s_min[256];
-    __shared__ int s_count;
-    if (t == 0) {
-        int mf = a.M - 1;
-        for (int m = 0; m < a.M; ++m)
-            if (a.lam[m] >= top) { mf = m; break; }
-        s_mfirst = mf;
-        s_count = 0;
-    }
+    if (threadIdx.x == 0) s_mf = a.M - 1;
     __syncthreads();
-    const int mlim = s_mfirst;
-    int kmax = a.K - 1;
+    for (int m = threadIdx.x; m < a.M; m += blockDim.x)
+        if (a.lam[m] >= top) atomicMin(&s_mf, m);
+    __syncthreads();
+    q.mlim = s_mf;
+    q.kmax = a.K - 1;
     if (a.k_max) {
-        kmax = a.k_max[c];
-        kmax = kmax < 0 ? 0 : (kmax > a.K - 1 ? a.K - 1 : kmax);
+        const int km = a.k_max[q.c];
+        q.kmax = km < 0 ? 0 : (km > a.K - 1 ? a.K - 1 : km);
     }
-    const double ev = (double)a.eps[(long long)e * a.C + c];
-    const long long npair = (long long)(kmax + 1) * (mlim + 1);
-    const double *Sc = a.S + (long long)c * a.K * a.M;
+    const int s = seg_of_x(a.seg, q.c);
+    q.ninv = 1.0 / (double)(a.offsets[s + 1] - a.offsets[s]);
+    q.ev = (double)a.eps[(long long)e * a.C + q.c];
+    q.slack = 1e-12 * (double)(cp + cw) * (double)a.L[q.c];
+    return q;
+}
 
-    double lmin = __builtin_inf();
-    for (long long i = t; i < npair; i += 256) {
-        const int k = (int)(i / (mlim + 1)), m = (int)(i % (mlim + 1));
-        const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
-                                   __ddiv_rn(Sc[(long long)k * a.M + m], N));
-        lmin = J < lmin ? J : lmin;
-    }
-    s_min[t] = lmin;
+__device__ __forceinline__ double approx_J(const BandArgs &a, const BandProblem &q, int k, int m)
+{
+    return (double)a.lam[m] * q.ev + a.S[((long long)q.c * a.K + k) * a.M + m] * q.ninv;
+}
+
+__device__ double block_min(double v)
+{
+    __shared__ double sm[256];
+    const int t = threadIdx.x;
+    sm[t] = v;
     __syncthreads();
     for (int w = 128; w > 0; w >>= 1) {
-        if (t < w) s_min[t] = s_min[t + w] < s_min[t] ? s_min[t + w] : s_min[t];
+        if (t < w) sm[t] = sm[t + w] < sm[t] ? sm[t + w] : sm[t];
         __syncthreads();
     }
-    const double wmin = s_min[0];
-    const double slack = 1e-12 * (double)(cp + cw) * (double)a.L[c];
-    const double T = wmin + kBandTau * wmin + slack;
+    const double r = sm[0];
+    __syncthreads();
+    return r;
+}
 
-    for (long long i = t; i < npair; i += 256) {
-        const int k = (int)(i / (mlim + 1)), m = (int)(i % (mlim + 1));
-        const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
-                                   __ddiv_rn(Sc[(long long)k * a.M + m], N));
-        if (J <= T) {
-            const int slot = atomicAdd(&s_count, 1);
+__global__ __launch_bounds__(256) void band_min_kernel(BandArgs a, double *chunk_min, int nchunks)
+{
+    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
+    const BandProblem q = band_problem(a, ec);
+    const int k0 = blockIdx.y * kBandKC;
+    const int k1 = min(k0 + kBandKC - 1, q.kmax);
+    const int nm = q.mlim + 1;
+    const int npair = k1 >= k0 ? (k1 - k0 + 1) * nm : 0;
+    double lmin = __builtin_inf();
+    for (int i = threadIdx.x; i < npair; i += 256) {
+        const double J = approx_J(a, q, k0 + i / nm, i % nm);
+        lmin = J < lmin ? J : lmin;
+    }
+    const double r = block_min(lmin);
+    if (threadIdx.x == 0) chunk_min[(long long)ec * nchunks + blockIdx.y] = r;
+}
+
+__global__ __launch_bounds__(256) void band_collect_kernel(BandArgs a, const double *chunk_min,
+                                                           int nchunks)
+{
+    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
+    const BandProblem q = band_problem(a, ec);
+    double lmin = __builtin_inf();
+    for (int i = threadIdx.x; i < nchunks; i += 256) {
+        const double v = chunk_min[(long long)ec * nchunks + i];
+        lmin = v < lmin ? v : lmin;
+    }
+    const double wmin = block_min(lmin);
+    const double T = wmin + kBandTau * wmin + q.slack;
+    const int k0 = blockIdx.y * kBandKC;
+    const int k1 = min(k0 + kBandKC - 1, q.kmax);
+    const int nm = q.mlim + 1;
+    const int npair = k1 >= k0 ? (k1 - k0 + 1) * nm : 0;
+    for (int i = threadIdx.x; i < npair; i += 256) {
+        const int k = k0 + i / nm, m = i % nm;
+        if (approx_J(a, q, k, m) <= T) {
+            const int slot = atomicAdd(&a.count[ec], 1);
             if (slot < kBandCap) a.cand[(long long)ec * kBandCap + slot] = k * a.M + m;
         }
     }
-    __syncthreads();
-    if (t == 0) {
-        int n = s_count;
-        if (n > kBandCap) {
-            atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_FULL);
-            n = kBandCap;
-        }
-        a.count[ec] = n;
-        a.thresh[ec] = T;
-    }
+    if (blockIdx.y == 0 && threadIdx.x == 0) a.thresh[ec] = T;
 }
 
-hipError_t launch_band(const BandArgs &a, hipStream_t st)
+hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st)
 {
-    const int blocks = a.c_only >= 0 ? 1 : a.E * a.C;
-    hipLaunchKernelGGL(band_kernel, dim3(blocks), dim3(256), 0, st, a);
+    const int nchunks = (a.K + kBandKC - 1) / kBandKC;
+    const int EC = a.c_only >= 0 ? 1 : a.E * a.C;
+    int32_t *count = a.count + (a.c_only >= 0 ? (a.e_row * a.C + a.c_only) : 0);
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((EC + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<uint32_t *>(count), (long long)EC, 0u);
+    hipLaunchKernelGGL(band_min_kernel, dim3(EC, nchunks), dim3(256), 0, st, a, chunk_min, nchunks);
+    hipLaunchKernelGGL(band_collect_kernel, dim3(EC, nchunks), dim3(256), 0, st, a,
+                       (const double *)chunk_min, nchunks);
     return hipGetLastError();
 }
 
@@ -158,7 +204,7 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineArgs a)
     const long long lo = n0 + (N * p) / a.P, hi = n0 + (N * (p + 1)) / a.P;
     const int64_t CP = fix33(a.c_p[c]), CW = fix33(a.c_w[c]);
     const int64_t L = a.L[c];
-    const int cnt = a.count[ec];
+    const int cnt = min(a.count[ec], kBandCap);
 
     __shared__ uint64_t s_lo[256], s_hi[256];
     for (int i = 0; i < cnt; ++i) {
@@ -210,7 +256,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalArgs a)
     const int s = seg_of_x(a.seg, c);
     const double N = (double)(a.offsets[s + 1] - a.offsets[s]);
     const double ev = (double)a.eps[(long long)e * a.C + c];
-    const int cnt = a.count[ec];
+    const int raw = a.count[ec];
+    const int cnt = min(raw, kBandCap);
 
     double bJ = __builtin_inf();
     int bkey = 0x7fffffff;
@@ -251,6 +298,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalArgs a)
         // the exact optimum must sit well inside the screening band
         const double T = a.thresh[ec];
         if (!(sJ[0] * (1.0 + 0.5 * kBandTau) < T) || cnt == 0) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_MARGIN);
+        if (raw > kBandCap) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_FULL);
     }
 }
 
@@ -262,12 +310,6 @@ hipError_t launch_finalize(const FinalArgs &a, hipStream_t st)
 }
 
 // -------------------------------------------------------------- quantile ----
-__global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
-{
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = v;
-}
-
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 {
     if (n <= 0) return hipSuccess;
@@ -383,14 +425,17 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
 // Grid indices arriving from the caller (k_prev) are clamped into [0, K).
 __device__ __forceinline__ int clampk(int k, int K) { return k < 0 ? 0 : (k >= K ? K - 1 : k); }
 
-// Alg. 1 initialisation: largest k with eta[k] * N <= sum of the samples.
-__global__ __launch_bounds__(256) void bcd_init_kernel(const int64_t *offsets, const int32_t *seg,
-                                                       const int32_t *xi, const int32_t *eta, int K,
-                                                       int32_t *k0)
+// Alg. 1 initialisation r0 = L_in + E[xi]: per class, the exact integer sum of
+// the samples (block partial sums added atomically; integer addition makes the
+// result independent of the order), then the largest k with eta[k] N <= sum.
+__global__ __launch_bounds__(256) void class_sum_kernel(const int64_t *offsets, const int32_t *seg,
+                                                        const int32_t *xi, long long chunk,
+                                                        unsigned long long *sums)
 {
     const int c = blockIdx.x, t = threadIdx.x;
     const int s = seg_of_x(seg, c);
-    const long long n0 = offsets[s], n1 = offsets[s + 1];
+    const long long n0 = offsets[s] + (long long)blockIdx.y * chunk;
+    const long long n1 = min(offsets[s + 1], n0 + chunk);
     long long sum = 0;
     for (long long n = n0 + t; n < n1; n += 256) sum += xi[n];
     __shared__ long long sh[256];
@@ -400,19 +445,38 @@ __global__ __launch_bounds__(256) void bcd_init_kernel(const int64_t *offsets, c
         if (t < w) sh[t] += sh[t + w];
         __syncthreads();
     }
-    if (t == 0) {
-        const long long tot = sh[0], N = n1 - n0;
-        int best = 0;
-        for (int k = 0; k < K; ++k)
-            if ((long long)eta[k] * N <= tot) best = k;
-        k0[c] = best;
+    if (t == 0 && sh[0] != 0) atomicAdd(&sums[c], (unsigned long long)sh[0]);
+}
+
+__global__ void bcd_init_select_kernel(const int64_t *offsets, const int32_t *seg, const int32_t *eta,
+                                       int C, int K, const unsigned long long *sums, int32_t *k0)
+{
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    const int s = seg_of_x(seg, c);
+    const long long N = offsets[s + 1] - offsets[s];
+    const long long tot = (long long)sums[c];
+    int lo = 0, hi = K - 1;  // eta ascending: largest k with eta[k] * N <= tot (0 if none)
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if ((long long)eta[mid] * N <= tot) lo = mid;
+        else hi = mid - 1;
     }
+    k0[c] = lo;
 }
 
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
-                           const int32_t *eta, int C, int K, int32_t *k0, hipStream_t st)
+                           const int32_t *eta, int C, int K, long long max_n,
+                           unsigned long long *sums, int32_t *k0, hipStream_t st)
 {
-    hipLaunchKernelGGL(bcd_init_kernel, dim3(C), dim3(256), 0, st, offsets, seg, xi, eta, K, k0);
+    const long long chunk = 1 << 16;
+    const long long nch = std::max(1LL, (max_n + chunk - 1) / chunk);
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((2 * C + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<uint32_t *>(sums), (long long)2 * C, 0u);
+    hipLaunchKernelGGL(class_sum_kernel, dim3(C, (unsigned)nch), dim3(256), 0, st, offsets, seg, xi,
+                       chunk, sums);
+    hipLaunchKernelGGL(bcd_init_select_kernel, dim3((C + 255) / 256), dim3(256), 0, st, offsets, seg,
+                       eta, C, K, (const unsigned long long *)sums, k0);
     return hipGetLastError();
 }
 
@@ -438,9 +502,17 @@ __global__ void bcd_kmax_kernel(const int32_t *eta, int C, int K, int G, const f
         const double b = __ddiv_rn(num, den);
         bound = b < bound ? b : bound;
     }
-    int km = -1;
-    for (int k = 0; k < K; ++k)
-        if ((double)eta[k] <= bound) km = k;
+    // eta ascending: the largest k with eta[k] <= bound, or none
+    int km = -1, lo = 0, hi = K - 1;
+    while (lo <= hi) {
+        const int mid = (lo + hi) / 2;
+        if ((double)eta[mid] <= bound) {
+            km = mid;
+            lo = mid + 1;
+        } else {
+            hi = mid - 1;
+        }
+    }
     feasible[c] = km >= 0 ? 1 : 0;
     kmax[c] = km >= 0 ? km : 0;
 }
