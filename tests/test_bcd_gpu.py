@@ -86,3 +86,33 @@ def test_cfg5_iterations_against_stored_oracle(ctx, dev):
         assert g["feasible"].tolist() == row["feasible"]
         assert g["q_value"].tolist() == row["q_value"]
         k_prev = g["k_next"]
+
+
+def _cfg5_tight(n=50_000, cap_scale=0.3):
+    """The drifting 8-class workload's grid, costs and routing, the first n
+    samples of each class, and capacities scaled down so that groups bind."""
+    from workloads.configs import Workload, Groups
+    w = make_workload("cfg5", iteration=0)
+    parts = [w.samples_of(c)[:n].copy() for c in range(w.C)]
+    off = np.zeros(w.C + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in parts])
+    g = Groups((w.groups.cap * np.float32(cap_scale)).astype(np.float32), w.groups.conc.copy(),
+               w.groups.kappa)
+    return Workload("cfg5-tight", w.C, off, None, np.concatenate(parts), w.L, w.eta, w.lam,
+                    w.c_p, w.c_w, 1, w.eps.copy(), groups=g)
+
+
+def test_block_step_with_binding_capacity_at_full_grid(ctx, dev):
+    w = _cfg5_tight()
+    k0, g, flags = gpu_step(ctx, w, dev)
+    assert flags == 0
+    S = oracle.S_exact(w)
+    W, _ = oracle.W_table(w, S)
+    o = oracle.bcd_step(w, W[0], k0)
+    assert np.array_equal(g["k_next"], o["k_next"])
+    assert np.array_equal(g["W_star"].view(np.uint64), o["W_star"].view(np.uint64))
+    assert np.array_equal(g["usage"].view(np.uint64), o["usage"].view(np.uint64))
+    assert np.array_equal(g["feasible"], o["feasible"])
+    # the sweep must have been limited by capacity somewhere
+    unconstrained, _ = oracle.argmin(W)
+    assert not np.array_equal(o["k_next"], unconstrained[0]), "no capacity bound was active"
