@@ -295,15 +295,39 @@ int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, cons
     return DRO_OK;
 }
 
-int run_quantile(dro_ctx *ctx, const dro_problem *p, uint32_t *hist, int32_t *q_value,
-                 int64_t *q_rank, hipStream_t st)
+long long max_segment(const dro_problem *p)
 {
     long long max_seg = 0;
     for (int s = 0; s < p->S; ++s)
         max_seg = std::max(max_seg, (long long)(p->offsets_h[s + 1] - p->offsets_h[s]));
-    HIPCHK(launch_fill_u32(hist, (long long)p->S * kHistBins, 0u, st));
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, max_seg, hist, st));
-    HIPCHK(launch_select(p->offsets, p->seg, p->c_p, p->c_w, hist, p->C, q_value, q_rank, st));
+    return max_seg;
+}
+
+struct QuantBufs {
+    uint32_t *hist, *part;
+    int B;
+};
+
+size_t quantile_bytes(const dro_problem *p, int num_cu)
+{
+    const int B = hist_parts(p->S, max_segment(p), num_cu);
+    return rup((size_t)p->S * kHistBins * 4) + (B > 1 ? rup((size_t)p->S * B * kHistBins * 4) : 0);
+}
+
+QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
+{
+    QuantBufs q;
+    q.B = hist_parts(p->S, max_segment(p), num_cu);
+    q.hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
+    q.part = q.B > 1 ? ar.take<uint32_t>((size_t)p->S * q.B * kHistBins) : nullptr;
+    return q;
+}
+
+int run_quantile(dro_ctx *ctx, const dro_problem *p, const QuantBufs &qb, int32_t *q_value,
+                 int64_t *q_rank, hipStream_t st)
+{
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_select(p->offsets, p->seg, p->c_p, p->c_w, qb.hist, p->C, q_value, q_rank, st));
     return DRO_OK;
 }
 
@@ -343,6 +367,11 @@ int dro_create(int hip_device, dro_ctx **out)
     if (hipGetDeviceProperties(&prop, hip_device) == hipSuccess && prop.multiProcessorCount > 0)
         ctx->num_cu = prop.multiProcessorCount;
     ctx->dense_bpc = dense_blocks_per_cu();
+    if (hist_prepare() != hipSuccess) {
+        (void)hipGetLastError();
+        delete ctx;
+        return DRO_EHIP;
+    }
     if (hipMalloc(&ctx->flags, sizeof(uint32_t)) != hipSuccess ||
         hipMemset(ctx->flags, 0, sizeof(uint32_t)) != hipSuccess) {
         delete ctx;
@@ -504,11 +533,11 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     if (!q_value || !q_rank) return fail(ctx, DRO_EINVAL, "q_value and q_rank must be non-NULL");
     DeviceGuard g(ctx->device);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, rup((size_t)p->S * kHistBins * 4), st);
+    rc = ensure_ws(ctx, quantile_bytes(p, ctx->num_cu), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
-    uint32_t *hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
-    return run_quantile(ctx, p, hist, q_value, q_rank, st);
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    return run_quantile(ctx, p, qb, q_value, q_rank, st);
 }
 
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream)
@@ -543,7 +572,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const int C = p->C;
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const int P = refine_slices(sh.max_n);
-    const size_t need = dense_bytes(p, pl, true) + rup((size_t)p->S * kHistBins * 4) +
+    const size_t need = dense_bytes(p, pl, true) + quantile_bytes(p, ctx->num_cu) +
                         refine_bytes(C, P, p->K) + rup((size_t)C * 8) + 3 * rup((size_t)C * 4);
     rc = ensure_ws(ctx, need, st);
     if (rc) return rc;
@@ -551,13 +580,13 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const size_t ckm = (size_t)C * p->K * p->M;
     double *S = ar.take<double>(ckm);
     double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
-    uint32_t *hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     RefineBufs rb = take_refine(ar, C, P, p->K);
     int64_t *q_rank = ar.take<int64_t>(C);
     int32_t *kmax = ar.take<int32_t>(C);
     int32_t *kcur = ar.take<int32_t>(C);
 
-    rc = run_quantile(ctx, p, hist, out->q_value, q_rank, st);
+    rc = run_quantile(ctx, p, qb, out->q_value, q_rank, st);
     if (rc) return rc;
     rc = run_dense(ctx, p, sh, S, part, pl, st);
     if (rc) return rc;

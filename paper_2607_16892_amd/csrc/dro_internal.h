@@ -112,10 +112,14 @@ hipError_t launch_finalize(const FinalArgs &a, hipStream_t st);
 
 // ---- quantile ----------------------------------------------------------------
 constexpr int kHistBins = 32769;   // values 0 .. 2^15
-constexpr int kHistChunk = 65535;  // samples per block (16-bit LDS counters)
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st);
-hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, long long max_seg,
-                            uint32_t *hist, hipStream_t st);
+// allows the histogram kernel its 128 KB of dynamic LDS (once per device)
+hipError_t hist_prepare();
+// blocks per segment for the histogram pass
+int hist_parts(int S, long long max_seg, int num_cu);
+// hist: [S][kHistBins]; part: [S][B][kHistBins] scratch (unused when B == 1)
+hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
+                            uint32_t *part, uint32_t *hist, hipStream_t st);
 hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st);

@@ -317,44 +317,97 @@ hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
     return hipGetLastError();
 }
 
-// Block (chunk, segment): counts of the values 0 .. 2^15 - 1 of up to
-// kHistChunk samples, two 16-bit counters per LDS word, flushed to the
-// segment's global histogram; the value 2^15 goes straight to global memory.
-__global__ __launch_bounds__(256) void histogram_kernel(const int64_t *offsets, const int32_t *xi,
-                                                        uint32_t *hist, int chunks)
+// Block (segment s, part b of B): a private 32-bit LDS histogram of the values
+// 0 .. 2^15 (128 KB) over its 1/B share of the segment, stored to
+// part[s][b][:] with plain coalesced writes (no global atomics, so segments
+// with many blocks do not serialise on the same counters); a second kernel sums
+// the B parts of each segment.  1024 threads per block, each with four 16-byte
+// loads in flight, so the pass streams from HBM.
+constexpr int kHistThreads = 1024;
+
+__global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *offsets,
+                                                                 const int32_t *xi, int B,
+                                                                 uint32_t *part)
 {
-    constexpr int kWords = (kHistBins - 1) / 2;
-    __shared__ uint32_t h[kWords];
-    const int s = (int)(blockIdx.x / chunks);
-    const long long chunk = blockIdx.x % chunks;
-    const long long n0 = offsets[s], n1 = offsets[s + 1];
-    const long long lo = n0 + chunk * kHistChunk;
-    if (lo >= n1) return;
-    const long long hi = min(n1, lo + kHistChunk);
-    uint32_t *g = hist + (long long)s * kHistBins;
-    for (int i = threadIdx.x; i < kWords; i += 256) h[i] = 0;
+    extern __shared__ uint32_t h[];  // kHistBins words
+    const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
+    const long long n0 = offsets[s], N = offsets[s + 1] - n0;
+    const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
+    const int t = threadIdx.x;
+    for (int i = t; i < kHistBins; i += kHistThreads) h[i] = 0;
     __syncthreads();
-    for (long long n = lo + threadIdx.x; n < hi; n += 256) {
-        int v = xi[n];
+    auto count = [&](int v) {
         v = v < 0 ? 0 : (v > kHistBins - 1 ? kHistBins - 1 : v);
-        if (v == kHistBins - 1) atomicAdd(&g[v], 1u);
-        else atomicAdd(&h[v >> 1], 1u << ((v & 1) * 16));
+        atomicAdd(&h[v], 1u);
+    };
+    // unaligned head (up to the first 16-byte aligned address), 16-byte body, tail
+    const long long mis = (long long)((reinterpret_cast<uintptr_t>(xi + lo) >> 2) & 3u);
+    const long long a0 = min(hi, lo + ((4 - mis) & 3));
+    const long long a1 = a0 + ((hi - a0) & ~3LL);
+    for (long long n = lo + t; n < a0; n += kHistThreads) count(xi[n]);
+    const int4 *v4 = reinterpret_cast<const int4 *>(xi + a0);
+    const long long nv = (a1 - a0) / 4;
+    for (long long r0 = 0; r0 < nv; r0 += 4LL * kHistThreads) {
+        int4 q[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const long long i = r0 + r * kHistThreads + t;
+            q[r] = i < nv ? v4[i] : make_int4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            if (r0 + r * kHistThreads + t >= nv) continue;
+            count(q[r].x);
+            count(q[r].y);
+            count(q[r].z);
+            count(q[r].w);
+        }
     }
+    for (long long n = a1 + t; n < hi; n += kHistThreads) count(xi[n]);
     __syncthreads();
-    for (int i = threadIdx.x; i < kWords; i += 256) {
-        const uint32_t w = h[i];
-        if (w & 0xffffu) atomicAdd(&g[2 * i], w & 0xffffu);
-        if (w >> 16) atomicAdd(&g[2 * i + 1], w >> 16);
-    }
+    uint32_t *o = part + ((long long)s * B + b) * kHistBins;
+    for (int i = t; i < kHistBins; i += kHistThreads) o[i] = h[i];
 }
 
-hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, long long max_seg,
-                            uint32_t *hist, hipStream_t st)
+// hist[s][v] = sum over b of part[s][b][v]
+__global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t *hist)
 {
-    const long long chunks = (max_seg + kHistChunk - 1) / kHistChunk;
-    if (chunks <= 0 || S <= 0) return hipSuccess;
-    hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)(chunks * S)), dim3(256), 0, st, offsets,
-                       xi, hist, (int)chunks);
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (long long)S * kHistBins) return;
+    const long long s = i / kHistBins, v = i % kHistBins;
+    const uint32_t *p = part + s * B * kHistBins + v;
+    uint32_t acc = 0;
+    for (int b = 0; b < B; ++b) acc += p[(long long)b * kHistBins];
+    hist[i] = acc;
+}
+
+hipError_t hist_prepare()
+{
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(histogram_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)(kHistBins * sizeof(uint32_t)));
+}
+
+int hist_parts(int S, long long max_seg, int num_cu)
+{
+    // about one resident block per compute unit, at least 16K samples per block
+    long long B = std::max(1LL, (long long)num_cu / std::max(S, 1));
+    B = std::min(B, std::max(1LL, max_seg / 16384));
+    return (int)B;
+}
+
+hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
+                            uint32_t *part, uint32_t *hist, hipStream_t st)
+{
+    if (S <= 0) return hipSuccess;
+    uint32_t *dst = B == 1 ? hist : part;
+    hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((long long)S * B)), dim3(kHistThreads),
+                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, dst);
+    if (B > 1) {
+        const long long n = (long long)S * kHistBins;
+        hipLaunchKernelGGL(hist_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                           (const uint32_t *)part, S, B, hist);
+    }
     return hipGetLastError();
 }
 
@@ -375,24 +428,26 @@ __device__ int64_t exact_rank(float cp, float cw, int64_t N)
 
 // Block per class: prefix counts over the segment histogram; the j-th
 // smallest sample is the first value whose cumulative count reaches j.
-__global__ __launch_bounds__(256) void select_kernel(const int64_t *offsets, const int32_t *seg,
-                                                     const float *c_p, const float *c_w,
-                                                     const uint32_t *hist, int32_t *q_value,
-                                                     int64_t *q_rank)
+constexpr int kSelThreads = 1024;
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offsets,
+                                                             const int32_t *seg, const float *c_p,
+                                                             const float *c_w, const uint32_t *hist,
+                                                             int32_t *q_value, int64_t *q_rank)
 {
     const int c = blockIdx.x, t = threadIdx.x;
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
     const int64_t j = exact_rank(c_p[c], c_w[c], N);
     const uint32_t *h = hist + (long long)s * kHistBins;
-    constexpr int per = (kHistBins + 255) / 256;
+    constexpr int per = (kHistBins + kSelThreads - 1) / kSelThreads;
     const int b0 = t * per, b1 = min(kHistBins, b0 + per);
     uint64_t part = 0;
     for (int v = b0; v < b1; ++v) part += h[v];
-    __shared__ uint64_t sc[256];
+    __shared__ uint64_t sc[kSelThreads];
     sc[t] = part;
     __syncthreads();
-    for (int w = 1; w < 256; w <<= 1) {  // inclusive scan
+    for (int w = 1; w < kSelThreads; w <<= 1) {  // inclusive scan
         const uint64_t add = t >= w ? sc[t - w] : 0;
         __syncthreads();
         sc[t] += add;
@@ -416,8 +471,8 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st)
 {
-    hipLaunchKernelGGL(select_kernel, dim3(C), dim3(256), 0, st, offsets, seg, c_p, c_w, hist,
-                       q_value, q_rank);
+    hipLaunchKernelGGL(select_kernel, dim3(C), dim3(kSelThreads), 0, st, offsets, seg, c_p, c_w,
+                       hist, q_value, q_rank);
     return hipGetLastError();
 }
 
