@@ -158,6 +158,22 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
 int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t *q_rank,
                    dro_stream_t stream);
 
+/* Exact table by value grouping and prefix sums.  For 0 <= x, eta <= L the three
+ * candidates of Step 4 reduce to the larger of two lines in x, so with the
+ * per-segment counts and sums of the sample values every S[c,k,m] is a closed
+ * form in 128-bit integers: O(N + L) per segment plus O(1) per (c,k,m), instead
+ * of O(N) per (c,k,m).  This is the production alternative to the dense
+ * evaluation when only the results are needed (it does not evaluate every
+ * per-sample term, so it is not the dense throughput measurement):
+ *   W[e,c,k], m_star[e,c,k] = exact-spec values (the expression of
+ *                             dro_argmin_reservation for every k), lowest m
+ *   k_star, W_star, m_at_star [E*C] = lowest-index optimum with k <= k_max[c]
+ *                             (k_star NULL: the argmin is skipped; m_at_star may be NULL).
+ * Uses C, S, offsets, seg, xi, L, eta, lam, c_p, c_w of `p`; k_max may be NULL. */
+int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
+                    const int32_t *k_max, double *W, int32_t *m_star, int32_t *k_star,
+                    double *W_star, int32_t *m_at_star, dro_stream_t stream);
+
 /* Initial state of Alg. 1: r0 = L_in + E[xi], i.e. k0[c] = the largest k with
  * eta[k] <= mean of the class samples (compared exactly). */
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream);

@@ -231,6 +231,32 @@ def dro_argmin_reservation(ctx: Context, prob: Problem, eps: torch.Tensor, S: to
     return dict(k_star=k_star, W_star=W_star, m_at_star=m_at_star)
 
 
+def dro_exact_table(ctx: Context, prob: Problem, eps: torch.Tensor,
+                    k_max: Optional[torch.Tensor] = None, want_argmin: bool = True,
+                    stream=None) -> dict:
+    """Exact W table, m_star and optimum from value counts (see dro_exact_table in dro.h)."""
+    dev = prob.device
+    _need_dev(eps, torch.float32, "eps", dev)
+    if k_max is not None:
+        _need_dev(k_max, torch.int32, "k_max", dev)
+    E = eps.numel() // prob.C
+    if E * prob.C != eps.numel() or E <= 0:
+        raise ValueError("eps must hold E*C radii")
+    W = torch.empty((E, prob.C, prob.K), dtype=torch.float64, device=dev)
+    m_star = torch.empty((E, prob.C, prob.K), dtype=torch.int32, device=dev)
+    k_star = W_star = m_at_star = None
+    if want_argmin:
+        k_star = torch.empty((E, prob.C), dtype=torch.int32, device=dev)
+        W_star = torch.empty((E, prob.C), dtype=torch.float64, device=dev)
+        m_at_star = torch.empty((E, prob.C), dtype=torch.int32, device=dev)
+    ps = prob.struct()
+    rc = ctx._lib.dro_exact_table(ctx.handle, ct.byref(ps), E, _ptr(eps), _ptr(k_max), _ptr(W),
+                                  _ptr(m_star), _ptr(k_star), _ptr(W_star), _ptr(m_at_star),
+                                  _stream(stream, dev))
+    ctx.check(rc, "dro_exact_table")
+    return dict(W=W, m_star=m_star, k_star=k_star, W_star=W_star, m_at_star=m_at_star)
+
+
 def class_quantile(ctx: Context, prob: Problem, q_value=None, q_rank=None, stream=None) -> dict:
     dev = prob.device
     q_value = _out(q_value, (prob.C,), torch.int32, dev, "q_value")

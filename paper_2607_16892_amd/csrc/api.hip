@@ -540,6 +540,31 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     return run_quantile(ctx, p, qb, q_value, q_rank, st);
 }
 
+int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
+                    const int32_t *k_max, double *W, int32_t *m_star, int32_t *k_star,
+                    double *W_star, int32_t *m_at_star, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
+    if (rc) return rc;
+    if (E <= 0 || !eps || !W || !m_star || (k_star && !W_star))
+        return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, m_star (and W_star with k_star) non-NULL");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const size_t bins = (size_t)p->S * kHistBins;
+    rc = ensure_ws(ctx, quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    uint32_t *cnt = ar.take<uint32_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(bins);
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, k_max,
+                              qb.hist, p->S, E, p->C, p->K, p->M, cnt, sum, W, m_star, k_star,
+                              W_star, m_at_star, st));
+    return DRO_OK;
+}
+
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream)
 {
     Shape sh;

@@ -124,6 +124,15 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st);
 
+// ---- exact table (value counts and prefix sums) -------------------------------
+// cnt: [S][kHistBins] u32, sum: [S][kHistBins] u64 scratch; k_star == null skips the argmin
+hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const int32_t *L,
+                              const int32_t *eta, const float *lam, const float *c_p,
+                              const float *c_w, const float *eps, const int32_t *k_max,
+                              const uint32_t *hist, int S, int E, int C, int K, int M,
+                              uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
+                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st);
+
 // ---- block step ----------------------------------------------------------------
 // sums: [C] scratch
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,

@@ -640,3 +640,186 @@ hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, i
 }
 
 }  // namespace dro
+
+namespace dro {
+
+// ============================================================ exact table ====
+// The whole table from value counts (the production alternative to the dense
+// pass when only results are needed; it does not evaluate per-sample terms).
+// For 0 <= x, eta <= L the three candidates of Step 4 reduce to the larger of
+// two lines, phi = max(B - a1 x, C - a2 (L - x)) with B = c_w eta,
+// C = c_p (L - eta), a1 = min(g, c_w), a2 = min(g, c_p); the first wins exactly
+// for (a1 + a2) x <= B - C + a2 L.  With the counts cnt(v) = #{x <= v} and sums
+// sum(v) = sum{x : x <= v} of the segment, and t the last sample value on the
+// first line's side,
+//   S = B cnt(t) - a1 sum(t) + (C - a2 L)(N - cnt(t)) + a2 (sum_all - sum(t)),
+// evaluated in 128-bit integers in units of 2^-33: exact.
+
+// Per segment: cnt[v] = #{x <= v} (u32) and sum[v] = sum of the samples <= v
+// (u64), from the value histogram; one 1024-thread block per segment.
+__global__ __launch_bounds__(1024) void prefix_kernel(const uint32_t *hist, uint32_t *cnt,
+                                                      uint64_t *sum)
+{
+    const int s = blockIdx.x, t = threadIdx.x;
+    constexpr int per = (kHistBins + 1023) / 1024;
+    const uint32_t *h = hist + (long long)s * kHistBins;
+    uint32_t *oc = cnt + (long long)s * kHistBins;
+    uint64_t *os = sum + (long long)s * kHistBins;
+    const int b0 = t * per, b1 = min(kHistBins, b0 + per);
+    uint64_t pc = 0, ps = 0;
+    for (int v = b0; v < b1; ++v) {
+        pc += h[v];
+        ps += (uint64_t)h[v] * (uint64_t)v;
+    }
+    __shared__ uint64_t sc[1024], ss[1024];
+    sc[t] = pc;
+    ss[t] = ps;
+    __syncthreads();
+    for (int w = 1; w < 1024; w <<= 1) {  // inclusive scans
+        const uint64_t ac = t >= w ? sc[t - w] : 0, as = t >= w ? ss[t - w] : 0;
+        __syncthreads();
+        sc[t] += ac;
+        ss[t] += as;
+        __syncthreads();
+    }
+    uint64_t c = sc[t] - pc, x = ss[t] - ps;
+    for (int v = b0; v < b1; ++v) {
+        c += h[v];
+        x += (uint64_t)h[v] * (uint64_t)v;
+        oc[v] = (uint32_t)c;
+        os[v] = x;
+    }
+}
+
+__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)  // b > 0
+{
+    int64_t q = a / b;
+    if ((a % b != 0) && (a < 0)) --q;
+    return q;
+}
+
+// Thread per (c, k): exact S for every m, exact J for every radius row, and
+// the minimum over m with the lowest m (W, m_star).
+__global__ __launch_bounds__(256) void exact_table_kernel(
+    const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
+    const float *lam, const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt,
+    const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star)
+{
+    const long long ck = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (ck >= (long long)C * K) return;
+    const int c = (int)(ck / K), k = (int)(ck % K);
+    const int s = seg_of_x(seg, c);
+    const int64_t N = offsets[s + 1] - offsets[s];
+    const int64_t L = L_[c], eta = eta_[k];
+    const uint32_t *cn = cnt + (long long)s * kHistBins;
+    const uint64_t *sm = sum + (long long)s * kHistBins;
+    const __int128 sum_all = (__int128)sm[kHistBins - 1];
+    const int64_t tmax = L < kHistBins - 1 ? L : kHistBins - 1;
+    const int64_t CP = fix33(c_p[c]), CW = fix33(c_w[c]);
+    const int64_t B = CW * eta, Cc = CP * (L - eta);
+    const double Nd = (double)N;
+    for (int e0 = 0; e0 < E; e0 += 8) {
+        double best[8];
+        int bm[8];
+        double ev[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            best[q] = __builtin_inf();
+            bm[q] = 0;
+            ev[q] = (e0 + q < E) ? (double)eps[(long long)(e0 + q) * C + c] : 0.0;
+        }
+        for (int m = 0; m < M; ++m) {
+            const int64_t G = fix33(lam[m]);
+            const int64_t A1 = G < CW ? G : CW, A2 = G < CP ? G : CP;
+            const int64_t num = B - Cc + A2 * L;
+            int64_t t = floor_div(num, A1 + A2);
+            t = t < -1 ? -1 : (t > tmax ? tmax : t);
+            const __int128 ct = t >= 0 ? (__int128)cn[t] : 0;
+            const __int128 st = t >= 0 ? (__int128)sm[t] : 0;
+            const __int128 S = (__int128)B * ct - (__int128)A1 * st +
+                               (__int128)(Cc - A2 * L) * ((__int128)N - ct) +
+                               (__int128)A2 * (sum_all - st);
+            const unsigned __int128 u = (unsigned __int128)S;
+            const double q_ = __ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), Nd);
+            const double lm = (double)lam[m];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const double J = __dadd_rn(__dmul_rn(lm, ev[q]), q_);
+                if (J < best[q]) {
+                    best[q] = J;
+                    bm[q] = m;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (e0 + q >= E) break;
+            const long long o = ((long long)(e0 + q) * C + c) * K + k;
+            W[o] = best[q];
+            m_star[o] = bm[q];
+        }
+    }
+}
+
+// Block per (e, c): lowest k <= kmax with the smallest W, and the values there.
+__global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, const int32_t *m_star,
+                                                           const int32_t *k_max, int C, int K,
+                                                           int32_t *k_star, double *W_star,
+                                                           int32_t *m_at_star)
+{
+    const int ec = blockIdx.x, c = ec % C, t = threadIdx.x;
+    int kmax = K - 1;
+    if (k_max) {
+        kmax = k_max[c];
+        kmax = kmax < 0 ? 0 : (kmax > K - 1 ? K - 1 : kmax);
+    }
+    const double *w = W + (long long)ec * K;
+    double bw = __builtin_inf();
+    int bk = 0x7fffffff;
+    for (int k = t; k <= kmax; k += 256)
+        if (w[k] < bw) {
+            bw = w[k];
+            bk = k;
+        }
+    __shared__ double sw[256];
+    __shared__ int sk[256];
+    sw[t] = bw;
+    sk[t] = bk;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if (t < s) {
+            const double w2 = sw[t + s];
+            const int k2 = sk[t + s];
+            if (w2 < sw[t] || (w2 == sw[t] && k2 < sk[t])) {
+                sw[t] = w2;
+                sk[t] = k2;
+            }
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        k_star[ec] = sk[0];
+        W_star[ec] = sw[0];
+        if (m_at_star) m_at_star[ec] = m_star[(long long)ec * K + sk[0]];
+    }
+}
+
+hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const int32_t *L,
+                              const int32_t *eta, const float *lam, const float *c_p,
+                              const float *c_w, const float *eps, const int32_t *k_max,
+                              const uint32_t *hist, int S, int E, int C, int K, int M,
+                              uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
+                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
+{
+    hipLaunchKernelGGL(prefix_kernel, dim3(S), dim3(1024), 0, st, hist, cnt, sum);
+    const long long n = (long long)C * K;
+    hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                       offsets, seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,
+                       (const uint64_t *)sum, E, C, K, M, W, m_star);
+    if (k_star)
+        hipLaunchKernelGGL(table_argmin_kernel, dim3(E * C), dim3(256), 0, st, (const double *)W,
+                           (const int32_t *)m_star, k_max, C, K, k_star, W_star, m_at_star);
+    return hipGetLastError();
+}
+
+}  // namespace dro

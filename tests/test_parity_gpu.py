@@ -167,3 +167,63 @@ def _kink_workload():
 def test_samples_on_the_kink(ctx, dev):
     w = _kink_workload()
     check_against_oracle(w, run_gpu(ctx, w, dev))
+
+
+# ------------------------------------------------------------ exact table ----
+# dro_exact_table (value counts and prefix sums) must reproduce the oracle's
+# exact-spec W table, m_star and optimum bit for bit, for every (e, c, k).
+
+def run_exact_table(ctx, w, dev, k_max=None):
+    import torch
+    import paper_2607_16892_amd as dro
+    print(f"[gpu] exact table {w.name} C={w.C} K={w.K} M={w.M} E={w.E}", flush=True)
+    prob = dro.Problem.from_workload(w, dev)
+    eps = torch.from_numpy(w.eps).to(dev)
+    km = None if k_max is None else torch.from_numpy(np.asarray(k_max, np.int32)).to(dev)
+    r = dro.dro_exact_table(ctx, prob, eps, k_max=km)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in r.items() if v is not None}
+
+
+def check_exact_table(w, g, kmax=None):
+    ref = oracle.solve(w, grouped=True, kmax=kmax)
+    assert np.array_equal(g["W"].view(np.uint64), ref["W"].view(np.uint64))
+    assert np.array_equal(g["m_star"], ref["m_star"])
+    assert np.array_equal(g["k_star"], ref["k_star"])
+    assert np.array_equal(g["W_star"].view(np.uint64), ref["W_star"].view(np.uint64))
+    assert np.array_equal(g["m_at_star"], ref["m_at_star"])
+
+
+@pytest.mark.parametrize("name", ["cfg1", "cfg2"])
+def test_exact_table_full_config(ctx, dev, name):
+    w = make_workload(name)
+    check_exact_table(w, run_exact_table(ctx, w, dev))
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=lambda c: f"seed{c['seed']}")
+def test_exact_table_random(ctx, dev, case):
+    w = random_workload(**case)
+    check_exact_table(w, run_exact_table(ctx, w, dev))
+
+
+def test_exact_table_kink_and_capacity(ctx, dev):
+    w = _kink_workload()
+    check_exact_table(w, run_exact_table(ctx, w, dev))
+    w = random_workload(seed=9, C=3, N=(300, 200, 100), L=800, K=65, M=17, E=2)
+    kmax = np.array([5, 64, 0], np.int32)
+    check_exact_table(w, run_exact_table(ctx, w, dev, k_max=kmax), kmax=kmax)
+
+
+@pytest.mark.parametrize("name", ["cfg3", "cfg4"])
+def test_exact_table_large_config_against_stored_oracle(ctx, dev, name):
+    gold = _golden(name)
+    w = make_workload(name)
+    assert w.checksum() == gold["checksum"]
+    g = run_exact_table(ctx, w, dev)
+    assert np.array_equal(g["k_star"], np.array(gold["k_star"]))
+    ws = np.array([[float.fromhex(v) for v in row] for row in gold["W_star"]])
+    assert np.array_equal(g["W_star"].view(np.uint64), ws.view(np.uint64))
+    assert np.array_equal(g["m_at_star"], np.array(gold["m_at_star"]))
+    for c, row in gold["W_rows"].items():
+        ref = np.array([float.fromhex(v) for v in row])
+        assert np.array_equal(g["W"][0, int(c)].view(np.uint64), ref.view(np.uint64)), f"class {c}"
