@@ -135,6 +135,28 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
 // Tiles of kTK x kTM pairs per lane; samples of a class split into P slices so
 // that the grid fills whole rounds of resident blocks (cap = CUs x blocks/CU):
 // the smallest P whose last round is at least 97 % full, slices >= 1024 samples.
+// The kernels index with the host-validated offsets and segment map: both are
+// copied into the workspace at the start of every call, so device data that
+// disagrees with the host copies can never steer a kernel outside xi.
+size_t stage_bytes(const dro_problem *p)
+{
+    return rup((size_t)(p->S + 1) * 8) + (p->seg_h ? rup((size_t)p->C * 4) : 0);
+}
+
+int stage_problem(dro_ctx *ctx, const dro_problem *p, Arena &ar, hipStream_t st, dro_problem *q)
+{
+    *q = *p;
+    int64_t *off = ar.take<int64_t>((size_t)p->S + 1);
+    HIPCHK(hipMemcpyAsync(off, p->offsets_h, (size_t)(p->S + 1) * 8, hipMemcpyHostToDevice, st));
+    q->offsets = off;
+    if (p->seg_h) {
+        int32_t *seg = ar.take<int32_t>((size_t)p->C);
+        HIPCHK(hipMemcpyAsync(seg, p->seg_h, (size_t)p->C * 4, hipMemcpyHostToDevice, st));
+        q->seg = seg;
+    }
+    return DRO_OK;
+}
+
 DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
 {
     DensePlan pl{};
@@ -491,9 +513,13 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     if (!g.ok) return fail(ctx, DRO_EHIP, "cannot select device %d", ctx->device);
     hipStream_t st = (hipStream_t)stream;
     const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
-    rc = ensure_ws(ctx, dense_bytes(p, pl, S == nullptr), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + dense_bytes(p, pl, S == nullptr), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
     const size_t ckm = (size_t)p->C * p->K * p->M;
     double *Sbuf = S ? S : ar.take<double>(ckm);
     double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
@@ -517,9 +543,13 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     hipStream_t st = (hipStream_t)stream;
     const int EC = E * p->C;
     const int P = refine_slices(sh.max_n);
-    rc = ensure_ws(ctx, refine_bytes(EC, P, p->K), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(EC, P, p->K), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
     RefineBufs rb = take_refine(ar, EC, P, p->K);
     return run_argmin(ctx, p, E, eps, S, k_max, 0, -1, rb, P, k_star, W_star, m_at_star, st);
 }
@@ -533,9 +563,13 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     if (!q_value || !q_rank) return fail(ctx, DRO_EINVAL, "q_value and q_rank must be non-NULL");
     DeviceGuard g(ctx->device);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, quantile_bytes(p, ctx->num_cu), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     return run_quantile(ctx, p, qb, q_value, q_rank, st);
 }
@@ -552,9 +586,13 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     DeviceGuard g(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
     uint64_t *sum = ar.take<uint64_t>(bins);
@@ -573,9 +611,13 @@ int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t
     if (!k0) return fail(ctx, DRO_EINVAL, "k0 must be non-NULL");
     DeviceGuard g(ctx->device);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, rup((size_t)p->C * 8), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + rup((size_t)p->C * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
     unsigned long long *sums = ar.take<unsigned long long>(p->C);
     HIPCHK(launch_bcd_init(p->offsets, p->seg, p->xi, p->eta, p->C, p->K, sh.max_n, sums, k0, st));
     return DRO_OK;
@@ -599,9 +641,13 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const int P = refine_slices(sh.max_n);
     const size_t need = dense_bytes(p, pl, true) + quantile_bytes(p, ctx->num_cu) +
                         refine_bytes(C, P, p->K) + rup((size_t)C * 8) + 3 * rup((size_t)C * 4);
-    rc = ensure_ws(ctx, need, st);
+    rc = ensure_ws(ctx, stage_bytes(p) + need, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
     const size_t ckm = (size_t)C * p->K * p->M;
     double *S = ar.take<double>(ckm);
     double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
