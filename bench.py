@@ -120,7 +120,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="cfg3")
-    ap.add_argument("--cpu-samples", type=int, default=8192)
+    ap.add_argument("--cpu-samples", type=int, default=81920)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--bcd-iters", type=int, default=3)
     ap.add_argument("--calibrate-copy", action="store_true",
