@@ -174,6 +174,18 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
                     const int32_t *k_max, double *W, int32_t *m_star, int32_t *k_star,
                     double *W_star, int32_t *m_at_star, dro_stream_t stream);
 
+/* Continuous-multiplier dual (eq. app_kantorovich with gamma >= 0 continuous,
+ * equal to the LP of Step 5 by strong duality, eq. app_strong_duality):
+ *   W[e,c,k]     = min over gamma >= 0 of gamma eps[e,c] + S(gamma) / N_c
+ *   gamma[e,c,k] = the smallest minimising gamma (in [0, max(c_p, c_w)])
+ * J is convex and piecewise linear in gamma; its right derivative follows from
+ * the per-segment value counts and sums, and a bisection finds the smallest
+ * minimiser; values are fp64 (relative error ~1e-12), not the exact-spec
+ * expression.  This removes the multiplier grid: W here is <= the grid W of
+ * dro_cost_eval, with equality when the grid holds the minimiser. */
+int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
+                        double *W, double *gamma, dro_stream_t stream);
+
 /* Initial state of Alg. 1: r0 = L_in + E[xi], i.e. k0[c] = the largest k with
  * eta[k] <= mean of the class samples (compared exactly). */
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream);

@@ -257,6 +257,22 @@ def dro_exact_table(ctx: Context, prob: Problem, eps: torch.Tensor,
     return dict(W=W, m_star=m_star, k_star=k_star, W_star=W_star, m_at_star=m_at_star)
 
 
+def dro_continuous_dual(ctx: Context, prob: Problem, eps: torch.Tensor, stream=None) -> dict:
+    """min over continuous gamma >= 0 of the dual, per (e, c, k) (see dro_continuous_dual in dro.h)."""
+    dev = prob.device
+    _need_dev(eps, torch.float32, "eps", dev)
+    E = eps.numel() // prob.C
+    if E * prob.C != eps.numel() or E <= 0:
+        raise ValueError("eps must hold E*C radii")
+    W = torch.empty((E, prob.C, prob.K), dtype=torch.float64, device=dev)
+    gamma = torch.empty((E, prob.C, prob.K), dtype=torch.float64, device=dev)
+    ps = prob.struct()
+    rc = ctx._lib.dro_continuous_dual(ctx.handle, ct.byref(ps), E, _ptr(eps), _ptr(W), _ptr(gamma),
+                                      _stream(stream, dev))
+    ctx.check(rc, "dro_continuous_dual")
+    return dict(W=W, gamma=gamma)
+
+
 def class_quantile(ctx: Context, prob: Problem, q_value=None, q_rank=None, stream=None) -> dict:
     dev = prob.device
     q_value = _out(q_value, (prob.C,), torch.int32, dev, "q_value")

@@ -603,6 +603,33 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     return DRO_OK;
 }
 
+int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
+                        double *W, double *gamma, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
+    if (rc) return rc;
+    if (E <= 0 || !eps || !W || !gamma)
+        return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, gamma non-NULL");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const size_t bins = (size_t)p->S * kHistBins;
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    uint32_t *cnt = ar.take<uint32_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(bins);
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_continuous_dual(p->offsets, p->seg, p->L, p->eta, p->c_p, p->c_w, eps, qb.hist,
+                                  p->S, E, p->C, p->K, cnt, sum, W, gamma, st));
+    return DRO_OK;
+}
+
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream)
 {
     Shape sh;

@@ -133,6 +133,13 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
                               int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st);
 
+// continuous-multiplier dual over the same prefix counts (gamma: the smallest minimiser)
+hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, const int32_t *L,
+                                  const int32_t *eta, const float *c_p, const float *c_w,
+                                  const float *eps, const uint32_t *hist, int S, int E, int C,
+                                  int K, uint32_t *cnt, uint64_t *sum, double *W, double *gamma,
+                                  hipStream_t st);
+
 // ---- block step ----------------------------------------------------------------
 // sums: [C] scratch
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,

@@ -823,3 +823,120 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
 }
 
 }  // namespace dro
+
+namespace dro {
+
+// ====================================================== continuous dual ====
+// W(eta) = min over gamma >= 0 of gamma eps + S(gamma) / N, the Kantorovich
+// dual of eq. (app_kantorovich) with gamma continuous (= the LP of Step 5 by
+// strong duality).  With a1 = min(g, c_w), a2 = min(g, c_p) the per-sample sup
+// is max(B - a1 x, C - a2 (L - x)): convex and piecewise linear in g, so J is
+// too, and its right derivative at any g follows from the value counts:
+//   dS/dg = -[g < c_w] sum_{x < x0} x - [g < c_p] sum_{x > x0} (L - x)
+//           + (#{x = x0}) max(-[g < c_w] x0, -[g < c_p] (L - x0)).
+// Bisection on [0, max(c_p, c_w)] (where J' = eps >= 0) finds the smallest g
+// with J'(g+) >= 0, i.e. the smallest minimiser; J is evaluated there in fp64.
+
+struct SegStats {
+    const uint32_t *cnt;
+    const uint64_t *sum;
+    double N, SX;
+    int tmax;
+};
+
+__device__ __forceinline__ void side_stats(const SegStats &g, long long t, double &n, double &s)
+{
+    if (t < 0) { n = 0.0; s = 0.0; return; }
+    if (t > g.tmax) t = g.tmax;
+    n = (double)g.cnt[t];
+    s = (double)g.sum[t];
+}
+
+// value J(g) and right derivative J'(g+) for one (eta, L, costs, eps)
+__device__ void dual_at(const SegStats &st, double B, double C, double L, double cw, double cp,
+                        double ev, double g, double &J, double &dJ)
+{
+    const double a1 = g < cw ? g : cw, a2 = g < cp ? g : cp;
+    const double s12 = a1 + a2;
+    double x0 = s12 > 0.0 ? (B - C + a2 * L) / s12 : (B >= C ? 1e300 : -1e300);
+    const double tf = floor(x0 < -2.0 ? -2.0 : (x0 > L + 2.0 ? L + 2.0 : x0));
+    const long long t = (long long)tf;
+    double n1, s1;  // samples x <= t
+    side_stats(st, t, n1, s1);
+    // value: line 1 for x <= t, line 2 above (equal at a tie, so ties do not matter)
+    const double S = B * n1 - a1 * s1 + (C - a2 * L) * (st.N - n1) + a2 * (st.SX - s1);
+    J = g * ev + S / st.N;
+    // derivative: ties exactly at x0 take the larger slope
+    double nt = 0.0, xt = 0.0;
+    if (tf == x0 && t >= 0 && t <= st.tmax) {
+        double n0, s0;
+        side_stats(st, t - 1, n0, s0);
+        nt = n1 - n0;
+        xt = (double)t;
+        n1 = n0;
+        s1 = s0;
+    }
+    const double w1 = g < cw ? 1.0 : 0.0, w2 = g < cp ? 1.0 : 0.0;
+    const double n2 = st.N - n1 - nt, s2 = st.SX - s1 - nt * xt;
+    double dS = -w1 * s1 - w2 * (L * n2 - s2);
+    if (nt > 0.0) {
+        const double d1 = -w1 * xt, d2 = -w2 * (L - xt);
+        dS += nt * (d1 > d2 ? d1 : d2);
+    }
+    dJ = ev + dS / st.N;
+}
+
+__global__ __launch_bounds__(256) void continuous_dual_kernel(
+    const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
+    const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt, const uint64_t *sum,
+    int E, int C, int K, double *W, double *gamma)
+{
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (long long)E * C * K) return;
+    const int k = (int)(i % K);
+    const int ec = (int)(i / K), c = ec % C, e = ec / C;
+    const int s = seg_of_x(seg, c);
+    SegStats st;
+    st.cnt = cnt + (long long)s * kHistBins;
+    st.sum = sum + (long long)s * kHistBins;
+    st.N = (double)(offsets[s + 1] - offsets[s]);
+    st.SX = (double)st.sum[kHistBins - 1];
+    const int Li = L_[c];
+    st.tmax = Li < kHistBins - 1 ? Li : kHistBins - 1;
+    const double L = (double)Li, eta = (double)eta_[k];
+    const double cw = (double)c_w[c], cp = (double)c_p[c];
+    const double B = cw * eta, Cc = cp * (L - eta);
+    const double ev = (double)eps[(long long)e * C + c];
+    double J, dJ;
+    double lo = 0.0, hi = cw > cp ? cw : cp;
+    dual_at(st, B, Cc, L, cw, cp, ev, 0.0, J, dJ);
+    if (!(dJ >= 0.0)) {
+        for (int it = 0; it < 200 && hi - lo > 0.0; ++it) {
+            const double mid = 0.5 * (lo + hi);
+            if (mid <= lo || mid >= hi) break;
+            dual_at(st, B, Cc, L, cw, cp, ev, mid, J, dJ);
+            if (dJ >= 0.0) hi = mid;
+            else lo = mid;
+        }
+        dual_at(st, B, Cc, L, cw, cp, ev, hi, J, dJ);
+        lo = hi;
+    }
+    W[i] = J;
+    gamma[i] = lo;
+}
+
+hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, const int32_t *L,
+                                  const int32_t *eta, const float *c_p, const float *c_w,
+                                  const float *eps, const uint32_t *hist, int S, int E, int C,
+                                  int K, uint32_t *cnt, uint64_t *sum, double *W, double *gamma,
+                                  hipStream_t st)
+{
+    hipLaunchKernelGGL(prefix_kernel, dim3(S), dim3(1024), 0, st, hist, cnt, sum);
+    const long long n = (long long)E * C * K;
+    hipLaunchKernelGGL(continuous_dual_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                       offsets, seg, L, eta, c_p, c_w, eps, (const uint32_t *)cnt,
+                       (const uint64_t *)sum, E, C, K, W, gamma);
+    return hipGetLastError();
+}
+
+}  // namespace dro
