@@ -35,11 +35,12 @@ METRIC = "DRO cost evals/sec (class×r×λ×sample per s) + % fp32 VALU peak"
 VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 add/fma on MI355X
 
 # Hardware-counter figures of the dense kernel on the 16 x 1e6 workload, from
-# profiles/dense_kernel_cfg3_counters.md.  They describe one build of
-# csrc/dense.hip (identified by the hash prefix) and are reported as null for
-# any other source or workload.
+# profiles/dense_kernel_cfg3_counters.md.  They describe one version of the
+# dense kernel's code (csrc/dense.hip and csrc/dro_internal.h with comments and
+# layout stripped, identified by the hash prefix) and are reported as null for
+# any other code or workload.
 DENSE_COUNTERS = {
-    "dense_hip_sha256_16": "db6f935de6063d6b",
+    "dense_code_sha256_16": "d14f1f312636bd5b",
     "workload": "cfg3",
     "valu_instr_per_eval": 2.103,        # SQ_INSTS_VALU x 64 / evaluations
     "hbm_bytes_per_launch": 912119.9 * 1024,   # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
@@ -47,14 +48,25 @@ DENSE_COUNTERS = {
 }
 
 
-def _counters_for(workload: str):
+def dense_code_hash() -> str:
+    """Hash of the dense kernel's code with comments and whitespace removed."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2607_16892_amd", "csrc", "dense.hip")
+    import re
+    text = ""
+    for name in ("dense.hip", "dro_internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_16892_amd", "csrc", name)) as f:
+            text += f.read() + "\n"
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
+
+
+def _counters_for(workload: str):
     try:
-        h = hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+        h = dense_code_hash()
     except OSError:
         return None
-    if h != DENSE_COUNTERS["dense_hip_sha256_16"] or workload != DENSE_COUNTERS["workload"]:
+    if h != DENSE_COUNTERS["dense_code_sha256_16"] or workload != DENSE_COUNTERS["workload"]:
         return None
     return DENSE_COUNTERS
 

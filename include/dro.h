@@ -5,17 +5,17 @@
  * multiplier lam_m standing in for the Wasserstein dual variable gamma, and
  * historical output-length sample x_n, the per-sample worst-case cost
  *
- *   phi(eta, x, g) = max{ c_w eta - g x,                          eq. (phi_0)
- *                         c_p (x - eta)^+ + c_w (eta - x)^+,       eq. (phi_sample)
- *                         c_p (L - eta) - g (L - x) }              eq. (phi_max)
+ *   phi(eta, x, g) = max{ c_w eta - g x,                          candidate at 0
+ *                         c_p (x - eta)^+ + c_w (eta - x)^+,       candidate at the sample
+ *                         c_p (L - eta) - g (L - x) }              candidate at L_max
  *
  * (paper, Appendix A, Step 4; eta = r - L_in is the buffer of Prop. 4.2),
- * the sums S[c,k,m] = sum_n phi (Step 5, eq. app_obj), the dual values
- * J = lam_m eps + S / N_c (eq. app_kantorovich with gamma on a grid), their
+ * the sums S[c,k,m] = sum_n phi (Appendix A, Step 5), the dual values
+ * J = lam_m eps + S / N_c (the Kantorovich dual of Appendix A, Step 3, with gamma on a grid), their
  * minimum over m, the lowest-index argmin over k (the optimal reservation of
- * Prop. 4.2 on the grid), the critical-fractile quantile (eq.
- * critical_fractile) and one capacity-constrained reservation update of
- * Block 1 of Alg. 1 under eq. (capacity).
+ * Prop. 4.2 on the grid), the critical-fractile quantile (Prop. 4.2,
+ * eps = 0) and one capacity-constrained reservation update of
+ * Block 1 of Alg. 1 under the memory-capacity constraint (Sec. 3.4).
  *
  * Conventions, binding on every entry point:
  *  - Array arguments are DEVICE memory owned by the caller unless the field
@@ -126,7 +126,7 @@ int dro_validate(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps
 int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out);
 
 /* Dense evaluation (Appendix A, Steps 4-5) and the minimum over the
- * multiplier grid (eq. app_kantorovich):
+ * multiplier grid (Kantorovich dual, Appendix A, Step 3):
  *   S[c,k,m]  = sum over the samples of class c of phi(eta_k, x, lam_m)
  *               every (c,k,m,n) term in fp32, runs of at most 64 samples
  *               folded into fp64 in a fixed order (deterministic)
@@ -174,8 +174,8 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
                     const int32_t *k_max, double *W, int32_t *m_star, int32_t *k_star,
                     double *W_star, int32_t *m_at_star, dro_stream_t stream);
 
-/* Continuous-multiplier dual (eq. app_kantorovich with gamma >= 0 continuous,
- * equal to the LP of Step 5 by strong duality, eq. app_strong_duality):
+/* Continuous-multiplier dual (Kantorovich dual of Appendix A, Step 3, with
+ * gamma >= 0 continuous; equal to the LP of Step 5 by strong duality, Step 2):
  *   W[e,c,k]     = min over gamma >= 0 of gamma eps[e,c] + S(gamma) / N_c
  *   gamma[e,c,k] = the smallest minimising gamma (in [0, max(c_p, c_w)])
  * J is convex and piecewise linear in gamma; its right derivative follows from
@@ -190,7 +190,8 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
  * eta[k] <= mean of the class samples (compared exactly). */
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream);
 
-/* One reservation update of Block 1 of Alg. 1 under eq. (capacity):
+/* One reservation update of Block 1 of Alg. 1 under the memory-capacity
+ * constraint (Sec. 3.4):
  * class_quantile, dro_cost_eval with one radius row eps[C], then a
  * Gauss-Seidel sweep over c = 0..C-1 in order.  For class c, with the other
  * classes at their current grid points and for every group g with

@@ -91,7 +91,7 @@ def threads() -> int:
 
 
 def phi(eta, x, L, cp, cw, lam) -> float:
-    """fp64 phi of eq. (phi_0)-(phi_max)."""
+    """fp64 phi of App. A, Step 4 (three candidate points)."""
     return float(_load().oracle_phi(int(eta), int(x), int(L), float(cp), float(cw), float(lam)))
 
 

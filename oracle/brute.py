@@ -9,9 +9,9 @@ oracle uses:
                       scanning the support [0, L] on a fine rational grid
                       plus the kinks of the objective;
   * `worst_case_lp`   the primal worst-case expectation over the Wasserstein
-                      ball (eq. app_dro, W1 of eq. wasserstein_def), as a
+                      ball (Appendix A, Step 1: the ball and its W1 distance), as a
                       transport-plan linear program solved with HiGHS;
-  * `dual_exact`      min over gamma >= 0 of the dual of eq. app_kantorovich,
+  * `dual_exact`      min over gamma >= 0 of the Kantorovich dual (App. A, Step 3),
                       evaluated exactly at every breakpoint of the convex
                       piecewise-linear objective;
   * `saa_exact`       the empirical mean of the stochastic cost (Sec. 3.3).
@@ -58,7 +58,7 @@ def _phi_max3(eta, x, L, cp, cw, g):
 
 
 def dual_exact(eta, xs, L, cp, cw, eps):
-    """min over gamma >= 0 of the Kantorovich dual (eq. app_kantorovich), exactly.
+    """min over gamma >= 0 of the Kantorovich dual (App. A, Step 3), exactly.
 
     Each per-sample supremum is a max of lines in gamma, so the objective is
     convex piecewise linear in gamma; its minimum sits at gamma = 0 or at a

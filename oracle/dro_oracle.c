@@ -9,15 +9,15 @@
  *   Q(eta, x)       = c_p (x - eta)^+ + c_w (eta - x)^+          stochastic cost, Sec. 3.3,
  *                                                                 with L_in folded into eta = r - L_in
  *   phi(eta, x, g)  = max{ Q(eta,0) - g x,  Q(eta,x),  Q(eta,L) - g (L - x) }
- *                                                                 eq. (phi_0), (phi_sample), (phi_max)
+ *                                                                 App. A, Step 4 (candidates at 0, at the sample, at L_max)
  *   S[c,k,m]        = sum over the samples x of class c of phi(eta_k, x, lam_m)
- *                                                                 Step 5, eq. (app_obj) at theta = phi
- *   J[e,c,k,m]      = lam_m eps[e,c] + S[c,k,m] / N_c            eq. (app_kantorovich) on a grid of gamma
+ *                                                                 App. A, Step 5 (LP objective) at theta = phi
+ *   J[e,c,k,m]      = lam_m eps[e,c] + S[c,k,m] / N_c            App. A, Step 3 (Kantorovich dual) on a grid of gamma
  *   W[e,c,k]        = min over m of J, m* the lowest m attaining it
  *   k*[e,c]         = lowest k <= kmax_c attaining min over k of W     (Prop. 4.2: optimal r on the grid)
  *   j_c             = ceil(c_p N_c / (c_p + c_w)), q_value = j_c-th smallest sample
- *                                                                 eq. (critical_fractile), generalized inverse
- *   block step      = one reservation update of Block 1 of Alg. 1 under eq. (capacity),
+ *                                                                 Prop. 4.2, generalized inverse
+ *   block step      = one reservation update of Block 1 of Alg. 1 under the memory-capacity constraint (Sec. 3.4),
  *                     Gauss-Seidel over classes (a reading: the paper leaves the grid form open)
  *
  * Two evaluations of S are provided:
@@ -57,13 +57,13 @@ static inline int32_t seg_of(const int32_t *seg, int32_t c) { return seg ? seg[c
 
 /* ------------------------------------------------------------ fp64 dense -- */
 
-/* phi in double precision, written term by term from eq. (phi_0)-(phi_max). */
+/* phi in double precision, written term by term from App. A, Step 4. */
 double oracle_phi(int32_t eta, int32_t x, int32_t L, float cp, float cw, float lam)
 {
     double e = eta, xx = x, LL = L, p = cp, w = cw, g = lam;
-    double q_at_x = p * fmax(xx - e, 0.0) + w * fmax(e - xx, 0.0);   /* (phi_sample) */
-    double q_at_0 = w * fmax(e, 0.0) - g * xx;                         /* (phi_0)      */
-    double q_at_L = p * (LL - e) - g * (LL - xx);                      /* (phi_max)    */
+    double q_at_x = p * fmax(xx - e, 0.0) + w * fmax(e - xx, 0.0);   /* at the sample */
+    double q_at_0 = w * fmax(e, 0.0) - g * xx;                         /* at 0         */
+    double q_at_L = p * (LL - e) - g * (LL - xx);                      /* at L_max     */
     double r = q_at_x;
     if (q_at_0 > r) r = q_at_0;
     if (q_at_L > r) r = q_at_L;

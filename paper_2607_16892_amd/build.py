@@ -4,7 +4,7 @@
 
 Each translation unit is compiled for gfx950 with packed-FP32 instructions
 disabled; the exact / capacity translation units also disable FMA
-contraction so their double expressions round as written.
+contraction so every double expression is rounded exactly as written.
 """
 from __future__ import annotations
 

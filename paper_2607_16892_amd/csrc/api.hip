@@ -133,8 +133,8 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
 }
 
 // Tiles of kTK x kTM pairs per lane; samples of a class split into P slices so
-// that the grid fills whole rounds of resident blocks (cap = CUs x blocks/CU):
-// the smallest P whose last round is at least 97 % full, slices >= 1024 samples.
+// that the grid fills whole waves of resident blocks (cap = CUs x blocks/CU):
+// the smallest P whose last wave is at least 97 % full, slices >= 1024 samples.
 // The kernels index with the host-validated offsets and segment map: both are
 // copied into the workspace at the start of every call, so device data that
 // disagrees with the host copies can never steer a kernel outside xi.
@@ -173,8 +173,8 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     double best = -1.0;
     for (long long P = 1; P <= maxP; ++P) {
         const long long n = base * P;
-        const long long rounds = (n + cap - 1) / cap;
-        const double fill = (double)n / (double)(rounds * cap);
+        const long long waves = (n + cap - 1) / cap;
+        const double fill = (double)n / (double)(waves * cap);
         if (fill > best + 1e-9) {
             best = fill;
             bestP = P;

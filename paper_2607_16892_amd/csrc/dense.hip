@@ -1,6 +1,6 @@
 // Dense evaluation of the per-sample worst-case cost and its sums
 // (paper, Appendix A, Step 4 closed form and Step 5 sums), plus the minimum
-// over the multiplier grid (eq. app_kantorovich with gamma on a grid).
+// over the multiplier grid (the Kantorovich dual of Appendix A, Step 3, with gamma on a grid).
 //
 // Work: one (class, grid point, multiplier, sample) term per evaluation,
 // C * K * M * N_c terms in all.  This is max-plus arithmetic, not a dense

@@ -828,7 +828,7 @@ namespace dro {
 
 // ====================================================== continuous dual ====
 // W(eta) = min over gamma >= 0 of gamma eps + S(gamma) / N, the Kantorovich
-// dual of eq. (app_kantorovich) with gamma continuous (= the LP of Step 5 by
+// dual (Appendix A, Step 3) with gamma continuous (= the LP of Step 5 by
 // strong duality).  With a1 = min(g, c_w), a2 = min(g, c_p) the per-sample sup
 // is max(B - a1 x, C - a2 (L - x)): convex and piecewise linear in g, so J is
 // too, and its right derivative at any g follows from the value counts:

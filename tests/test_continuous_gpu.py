@@ -1,7 +1,7 @@
 """The continuous-multiplier dual (dro_continuous_dual) against exact rationals.
 
 The reference is oracle/brute.dual_exact: the Kantorovich dual of
-eq. (app_kantorovich) minimised over continuous gamma >= 0 by evaluating it,
+App. A, Step 3, minimised over continuous gamma >= 0 by evaluating it,
 in fractions, at every breakpoint (itself pinned to the HiGHS transport LP on
 the CPU).  At full size the checks are the grid bound (the grid dual can only
 be larger) and the SAA bound.

@@ -54,7 +54,7 @@ def test_P1_edges():
 
 
 # ---------------------------------------------------------------- P2 -------
-# Strong duality (eq. app_strong_duality) and the LP of Step 5: the
+# Strong duality (App. A, Step 2) and the LP of App. A, Step 5: the
 # transport-plan primal equals the continuous-gamma dual; the grid dual
 # (what the path computes) is an upper bound, tight when the grid holds the
 # minimising gamma.
