@@ -36,11 +36,11 @@ VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 
 
 # Hardware-counter figures of the dense kernel on the 16 x 1e6 workload, from
 # profiles/dense_kernel_cfg3_counters.md.  They describe one version of the
-# dense kernel's code (csrc/dense.hip and csrc/dro_internal.h with comments and
-# layout stripped, identified by the hash prefix) and are reported as null for
-# any other code or workload.
+# dense kernel's code (csrc/dense.hip and the constants of csrc/dro_internal.h,
+# comments and layout stripped, identified by the hash prefix) and are
+# reported as null for any other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "d14f1f312636bd5b",
+    "dense_code_sha256_16": "adef0dc54cbbaa9b",
     "workload": "cfg3",
     "valu_instr_per_eval": 2.103,        # SQ_INSTS_VALU x 64 / evaluations
     "hbm_bytes_per_launch": 912119.9 * 1024,   # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
@@ -52,12 +52,13 @@ def dense_code_hash() -> str:
     """Hash of the dense kernel's code with comments and whitespace removed."""
     import hashlib
     import re
-    text = ""
-    for name in ("dense.hip", "dro_internal.h"):
+    def code(name):
         with open(os.path.join(ROOT, "paper_2607_16892_amd", "csrc", name)) as f:
-            text += f.read() + "\n"
-    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-    text = re.sub(r"//[^\n]*", " ", text)
+            text = re.sub(r"/\*.*?\*/", " ", f.read(), flags=re.S)
+        return re.sub(r"//[^\n]*", " ", text)
+
+    consts = [ln for ln in code("dro_internal.h").splitlines() if "constexpr" in ln]
+    text = code("dense.hip") + "\n" + "\n".join(consts)
     return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
 
 

@@ -91,7 +91,7 @@ typedef struct {
     const float *c_w;         /* [C] waste cost per reserved, unused token (Sec. 3.3)           */
 } dro_problem;
 
-/* Serving groups for the capacity constraint (eq. capacity, no prefix caching). */
+/* Serving groups for the capacity constraint (the memory-capacity constraint of Sec. 3.4, no prefix caching). */
 typedef struct {
     int32_t G;
     const float *cap;         /* [G] KV capacity of each group, tokens (M_k)                    */
@@ -150,7 +150,7 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
                            const double *S, const int32_t *k_max, int32_t *k_star, double *W_star,
                            int32_t *m_at_star, dro_stream_t stream);
 
-/* Critical-fractile quantile per class (eq. critical_fractile at eps = 0,
+/* Critical-fractile quantile per class (Prop. 4.2 at eps = 0,
  * generalized inverse of the empirical CDF):
  *   q_rank[c]  = j = ceil(c_p N_c / (c_p + c_w)), computed exactly, in [1, N_c]
  *   q_value[c] = the j-th smallest sample of class c.
@@ -185,6 +185,31 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
  * dro_cost_eval, with equality when the grid holds the minimiser. */
 int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
                         double *W, double *gamma, dro_stream_t stream);
+
+/* Per-class sample moments, exact (the inputs of the mean-based reservation of
+ * Alg. 1's initial state and of the mean and mean-plus-spread baselines of
+ * Sec. 5.1 and Sec. 5.4):
+ *   count[c] = N_c,  sum[c] = sum of x,  sumsq[c] = sum of x^2,
+ *   xmax[c]  = the largest sample of class c.
+ * All outputs are device arrays of length C.  Uses C, S, offsets, seg, xi, L of
+ * `p` (the value histogram assumes validated samples, 0 <= x <= L <= 2^15). */
+int class_moments(dro_ctx *ctx, const dro_problem *p, int64_t *count, int64_t *sum,
+                  int64_t *sumsq, int32_t *xmax, dro_stream_t stream);
+
+/* Average stochastic cost of given reservations over each class's samples
+ * (the per-arrival preemption/waste cost of Sec. 3.3 with eta = r - L_in, by
+ * which Sec. 5.2 and Table 2 compare reservation policies):
+ *   cost[r*C + c]  = RN( RN(S) / N_c ),  S = sum_n Q(eta, x_n) exactly,
+ *                    Q(eta, x) = c_p (x - eta)^+ + c_w (eta - x)^+,
+ *   cover[r*C + c] = #{n : x_n <= eta}, the empirical level of eta,
+ * for eta = eta_r[r*C + c], r = 0..R-1.  eta_r is a device int32 array of
+ * R*C reservations (any integer: below 0 every sample is preempted, above the
+ * largest sample every one is waste); cost (double) and cover (int64) are
+ * device arrays of R*C.  Exact: the sum follows from the per-segment value
+ * counts and sums in 128-bit integers.  R >= 1 and all pointers non-NULL, else
+ * DRO_EINVAL.  Uses C, S, offsets, seg, xi, L, c_p, c_w of `p`. */
+int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const int32_t *eta_r,
+                         double *cost, int64_t *cover, dro_stream_t stream);
 
 /* Initial state of Alg. 1: r0 = L_in + E[xi], i.e. k0[c] = the largest k with
  * eta[k] <= mean of the class samples (compared exactly). */

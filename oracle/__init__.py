@@ -74,6 +74,10 @@ def _load():
             lib.oracle_bcd_step.argtypes = [i32, i32, P, P, i32, P, P, f32, P, P, P, P, P]
             lib.oracle_bcd_init.restype = None
             lib.oracle_bcd_init.argtypes = [i32, P, P, P, i32, P, P]
+            lib.oracle_moments.restype = None
+            lib.oracle_moments.argtypes = [i32, P, P, P, P, P, P, P]
+            lib.oracle_reservation_cost.restype = ct.c_int
+            lib.oracle_reservation_cost.argtypes = [i32, P, P, P, P, P, i32, P, P, P, P, P]
             _lib = lib
     return _lib
 
@@ -229,3 +233,32 @@ def solve(w, grouped: bool = True, kmax=None):
     E = W.shape[0]
     m_at = np.array([[ms[e, c, ks[e, c]] for c in range(w.C)] for e in range(E)], np.int32)
     return dict(S=S, W=W, m_star=ms, k_star=ks, W_star=ws, m_at_star=m_at, q_value=qv, q_rank=qr)
+
+
+def moments(w):
+    """Per class: count, sum, sum of squares and largest sample (exact integers)."""
+    off, seg, xi, L, eta, lam, cp, cw = _prob(w)
+    out = dict(count=np.empty(w.C, np.int64), sum=np.empty(w.C, np.int64),
+               sumsq=np.empty(w.C, np.int64), xmax=np.empty(w.C, np.int32))
+    _load().oracle_moments(w.C, _p(off), _p(seg), _p(xi), _p(out["count"]), _p(out["sum"]),
+                           _p(out["sumsq"]), _p(out["xmax"]))
+    return out
+
+
+def reservation_cost(w, eta_r):
+    """Average cost of reservations eta_r[R, C] over each class's samples.
+
+    Returns (cost [R, C] float64, cover [R, C] int64, exact sums as ExactS).
+    """
+    off, seg, xi, L, eta, lam, cp, cw = _prob(w)
+    eta_r = np.ascontiguousarray(eta_r, dtype=np.int32).reshape(-1, w.C)
+    R = eta_r.shape[0]
+    cost = np.empty((R, w.C), np.float64)
+    cover = np.empty((R, w.C), np.int64)
+    hi = np.empty((R, w.C), np.int64)
+    lo = np.empty((R, w.C), np.uint64)
+    rc = _load().oracle_reservation_cost(w.C, _p(off), _p(seg), _p(xi), _p(cp), _p(cw), R,
+                                         _p(eta_r), _p(cost), _p(cover), _p(hi), _p(lo))
+    if rc != 0:
+        raise ValueError("a coefficient is outside the exact fixed-point range")
+    return cost, cover, ExactS(hi, lo)

@@ -316,7 +316,8 @@ void oracle_quantile(int32_t C, const int64_t *offsets, const int32_t *seg, cons
 /* ----------------------------------------------------------- block step -- */
 
 /* Capacity bound of class c on every group it is routed to, given the other
- * classes' current grid points (eq. capacity, no prefix caching):
+ * classes' current grid points (the memory-capacity constraint of Sec. 3.4,
+ * no prefix caching):
  *   other_g = (1+kappa) * sum_{c' != c} conc[c',g] * eta[k[c']]   (ascending c')
  *   bound_g = (cap[g] - other_g) / ((1+kappa) * conc[c,g])
  * Returns the smallest bound over the groups with conc[c,g] > 0 (+inf if none). */
@@ -393,4 +394,70 @@ void oracle_bcd_init(int32_t C, const int64_t *offsets, const int32_t *seg, cons
             if ((i128)eta[k] * n <= (i128)sum) best = k;
         k0[c] = best;
     }
+}
+
+/* ----------------------------------------------- reservation cost, moments -- */
+
+/* Per class: number of samples, their sum, their sum of squares and the
+ * largest sample, in exact integers. */
+void oracle_moments(int32_t C, const int64_t *offsets, const int32_t *seg, const int32_t *xi,
+                    int64_t *count, int64_t *sum, int64_t *sumsq, int32_t *xmax)
+{
+    for (int32_t c = 0; c < C; ++c) {
+        int32_t s = seg_of(seg, c);
+        int64_t n = 0, a = 0, b = 0;
+        int32_t mx = 0;
+        for (int64_t i = offsets[s]; i < offsets[s + 1]; ++i) {
+            n += 1;
+            a += xi[i];
+            b += (int64_t)xi[i] * xi[i];
+            if (xi[i] > mx) mx = xi[i];
+        }
+        count[c] = n;
+        sum[c] = a;
+        sumsq[c] = b;
+        xmax[c] = mx;
+    }
+}
+
+/* Average stochastic cost of a reservation over the samples of a class
+ * (Sec. 3.3, the per-arrival preemption/waste cost of a reservation):
+ *   cost[r*C + c]  = RN( RN(S) / N_c ),  S = sum_n Q(eta, x_n) exactly,
+ *                    Q(eta, x) = c_p (x - eta)^+ + c_w (eta - x)^+,
+ *                    eta = eta_r[r*C + c], any integer;
+ *   cover[r*C + c] = #{n : x_n <= eta}   (the empirical level of eta).
+ * Every term is an exact multiple of 2^-33 and is summed in 128-bit integers
+ * in sample order.  Returns 0, or -1 if a cost is outside the fixed-point range. */
+int oracle_reservation_cost(int32_t C, const int64_t *offsets, const int32_t *seg,
+                            const int32_t *xi, const float *cp, const float *cw, int32_t R,
+                            const int32_t *eta_r, double *cost, int64_t *cover, int64_t *S_hi,
+                            uint64_t *S_lo)
+{
+    int ok = 1;
+    for (int32_t c = 0; c < C; ++c) { (void)to_fix(cp[c], &ok); (void)to_fix(cw[c], &ok); }
+    if (!ok) return -1;
+    int64_t total = (int64_t)R * C;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t rc = 0; rc < total; ++rc) {
+        int32_t c = (int32_t)(rc % C);
+        int32_t s = seg_of(seg, c);
+        int okl = 1;
+        i128 CP = to_fix(cp[c], &okl), CW = to_fix(cw[c], &okl);
+        i128 eta = eta_r[rc];
+        i128 acc = 0;
+        int64_t below = 0;
+        for (int64_t n = offsets[s]; n < offsets[s + 1]; ++n) {
+            i128 x = xi[n];
+            i128 q = CP * (x > eta ? x - eta : 0) + CW * (eta > x ? eta - x : 0);
+            acc += q;
+            if (x <= eta) below += 1;
+        }
+        int64_t N = offsets[s + 1] - offsets[s];
+        double sd = ldexp((double)acc, -FIX_SHIFT);
+        cost[rc] = sd / (double)N;
+        cover[rc] = below;
+        if (S_hi) S_hi[rc] = (int64_t)(acc >> 64);
+        if (S_lo) S_lo[rc] = (uint64_t)acc;
+    }
+    return 0;
 }

@@ -41,6 +41,8 @@ EXPORTS = {
     "class_quantile": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P, P]),
     "dro_exact_table": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P, P, P, P]),
     "dro_continuous_dual": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P]),
+    "class_moments": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P, P, P, P]),
+    "dro_reservation_cost": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P]),
     "bcd_init_state": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P]),
     "bcd_block_step": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, ct.POINTER(GroupsStruct), P,
                                   ct.POINTER(StepOutStruct), P]),

@@ -284,6 +284,36 @@ def class_quantile(ctx: Context, prob: Problem, q_value=None, q_rank=None, strea
     return dict(q_value=q_value, q_rank=q_rank)
 
 
+def class_moments(ctx: Context, prob: Problem, stream=None) -> dict:
+    """Per-class count, sum, sum of squares and largest sample (see class_moments in dro.h)."""
+    dev = prob.device
+    out = dict(count=torch.empty(prob.C, dtype=torch.int64, device=dev),
+               sum=torch.empty(prob.C, dtype=torch.int64, device=dev),
+               sumsq=torch.empty(prob.C, dtype=torch.int64, device=dev),
+               xmax=torch.empty(prob.C, dtype=torch.int32, device=dev))
+    ps = prob.struct()
+    rc = ctx._lib.class_moments(ctx.handle, ct.byref(ps), _ptr(out["count"]), _ptr(out["sum"]),
+                                _ptr(out["sumsq"]), _ptr(out["xmax"]), _stream(stream, dev))
+    ctx.check(rc, "class_moments")
+    return out
+
+
+def dro_reservation_cost(ctx: Context, prob: Problem, eta_r: torch.Tensor, stream=None) -> dict:
+    """Average cost of reservations eta_r[R, C] (see dro_reservation_cost in dro.h)."""
+    dev = prob.device
+    _need_dev(eta_r, torch.int32, "eta_r", dev)
+    R = eta_r.numel() // prob.C
+    if R * prob.C != eta_r.numel() or R <= 0:
+        raise ValueError("eta_r must hold R*C reservations")
+    cost = torch.empty((R, prob.C), dtype=torch.float64, device=dev)
+    cover = torch.empty((R, prob.C), dtype=torch.int64, device=dev)
+    ps = prob.struct()
+    rc = ctx._lib.dro_reservation_cost(ctx.handle, ct.byref(ps), R, _ptr(eta_r), _ptr(cost),
+                                       _ptr(cover), _stream(stream, dev))
+    ctx.check(rc, "dro_reservation_cost")
+    return dict(cost=cost, cover=cover)
+
+
 def bcd_init_state(ctx: Context, prob: Problem, k0=None, stream=None) -> torch.Tensor:
     dev = prob.device
     k0 = _out(k0, (prob.C,), torch.int32, dev, "k0")

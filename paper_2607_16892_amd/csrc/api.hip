@@ -630,6 +630,58 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     return DRO_OK;
 }
 
+int class_moments(dro_ctx *ctx, const dro_problem *p, int64_t *count, int64_t *sum,
+                  int64_t *sumsq, int32_t *xmax, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
+    if (rc) return rc;
+    if (!count || !sum || !sumsq || !xmax)
+        return fail(ctx, DRO_EINVAL, "count, sum, sumsq and xmax must be non-NULL");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_moments(p->seg, qb.hist, p->C, count, sum, sumsq, xmax, st));
+    return DRO_OK;
+}
+
+int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const int32_t *eta_r,
+                         double *cost, int64_t *cover, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
+    if (rc) return rc;
+    if (R <= 0 || !eta_r || !cost || !cover)
+        return fail(ctx, DRO_EINVAL, "R must be > 0 and eta_r, cost, cover non-NULL");
+    if ((long long)R * p->C > (1LL << 31))
+        return fail(ctx, DRO_ELIMIT, "R*C = %lld reservations exceed 2^31", (long long)R * p->C);
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const size_t bins = (size_t)p->S * kHistBins;
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    uint32_t *cnt = ar.take<uint32_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(bins);
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_reservation_cost(p->offsets, p->seg, p->c_p, p->c_w, qb.hist, p->S, p->C, R,
+                                   eta_r, cnt, sum, cost, cover, st));
+    return DRO_OK;
+}
+
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream)
 {
     Shape sh;

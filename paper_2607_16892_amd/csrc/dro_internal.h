@@ -140,6 +140,14 @@ hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, co
                                   int K, uint32_t *cnt, uint64_t *sum, double *W, double *gamma,
                                   hipStream_t st);
 
+// ---- reservation cost and class moments ----------------------------------------
+hipError_t launch_moments(const int32_t *seg, const uint32_t *hist, int C, int64_t *count,
+                          int64_t *sum, int64_t *sumsq, int32_t *xmax, hipStream_t st);
+hipError_t launch_reservation_cost(const int64_t *offsets, const int32_t *seg, const float *c_p,
+                                   const float *c_w, const uint32_t *hist, int S, int C, int R,
+                                   const int32_t *eta_r, uint32_t *cnt, uint64_t *sum,
+                                   double *cost, int64_t *cover, hipStream_t st);
+
 // ---- block step ----------------------------------------------------------------
 // sums: [C] scratch
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,

@@ -535,7 +535,7 @@ hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int
     return hipGetLastError();
 }
 
-// Capacity bound of class c (eq. capacity), then the largest admissible k.
+// Capacity bound of class c (the memory-capacity constraint of Sec. 3.4), then the largest admissible k.
 __global__ void bcd_kmax_kernel(const int32_t *eta, int C, int K, int G, const float *cap,
                                 const float *conc, float kappa, const int32_t *kcur, int c,
                                 int32_t *kmax, uint8_t *feasible)
@@ -936,6 +936,116 @@ hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, co
     hipLaunchKernelGGL(continuous_dual_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                        offsets, seg, L, eta, c_p, c_w, eps, (const uint32_t *)cnt,
                        (const uint64_t *)sum, E, C, K, W, gamma);
+    return hipGetLastError();
+}
+
+}  // namespace dro
+
+namespace dro {
+
+// ===================================================== reservation cost ====
+// The stochastic cost of Sec. 3.3, Q(eta, x) = c_p (x - eta)^+ + c_w (eta - x)^+,
+// averaged over a class's samples for any given reservations, and the class
+// moments from which mean- and spread-based reservations are formed.  Both
+// read the value histogram: with cnt(v) = #{x <= v} and sum(v) the sum of
+// those samples, for an integer eta
+//   sum_n Q(eta, x_n) = c_p ((SX - sum(eta)) - eta (N - cnt(eta)))
+//                     + c_w (eta cnt(eta) - sum(eta)),
+// evaluated in 128-bit integers in units of 2^-33: exact for every eta.
+
+// One block per class: count, sum, sum of squares and largest sample.
+__global__ __launch_bounds__(1024) void moments_kernel(const int32_t *seg, const uint32_t *hist,
+                                                       int64_t *count, int64_t *sum,
+                                                       int64_t *sumsq, int32_t *xmax)
+{
+    const int c = blockIdx.x, t = threadIdx.x;
+    const uint32_t *h = hist + (long long)seg_of_x(seg, c) * kHistBins;
+    unsigned long long n = 0, a = 0, b = 0;
+    int mx = -1;
+    for (int v = t; v < kHistBins; v += 1024) {
+        const unsigned long long k = h[v];
+        n += k;
+        a += k * (unsigned long long)v;
+        b += k * (unsigned long long)v * (unsigned long long)v;
+        if (k) mx = v;  // ascending within a thread
+    }
+    __shared__ unsigned long long sn[1024], sa[1024], sb[1024];
+    __shared__ int sm[1024];
+    sn[t] = n;
+    sa[t] = a;
+    sb[t] = b;
+    sm[t] = mx;
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+        if (t < w) {
+            sn[t] += sn[t + w];
+            sa[t] += sa[t + w];
+            sb[t] += sb[t + w];
+            sm[t] = max(sm[t], sm[t + w]);
+        }
+        __syncthreads();
+    }
+    if (t == 0) {
+        count[c] = (int64_t)sn[0];
+        sum[c] = (int64_t)sa[0];
+        sumsq[c] = (int64_t)sb[0];
+        xmax[c] = sm[0] < 0 ? 0 : sm[0];
+    }
+}
+
+// Thread per (row r, class c): cost = RN(RN(S) / N) and cover = cnt(eta).
+__global__ __launch_bounds__(256) void reservation_cost_kernel(
+    const int64_t *offsets, const int32_t *seg, const float *c_p, const float *c_w,
+    const uint32_t *cnt, const uint64_t *sum, int C, long long RC, const int32_t *eta_r,
+    double *cost, int64_t *cover)
+{
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= RC) return;
+    const int c = (int)(i % C);
+    const int s = seg_of_x(seg, c);
+    const int64_t N = offsets[s + 1] - offsets[s];
+    const uint32_t *cn = cnt + (long long)s * kHistBins;
+    const uint64_t *sm = sum + (long long)s * kHistBins;
+    const __int128 SX = (__int128)sm[kHistBins - 1];
+    const int64_t eta = eta_r[i];
+    int64_t nle;
+    __int128 sle;
+    if (eta < 0) {
+        nle = 0;
+        sle = 0;
+    } else if (eta >= kHistBins - 1) {
+        nle = N;
+        sle = SX;
+    } else {
+        nle = (int64_t)cn[eta];
+        sle = (__int128)sm[eta];
+    }
+    const __int128 CP = fix33(c_p[c]), CW = fix33(c_w[c]);
+    const __int128 S = CP * ((SX - sle) - (__int128)eta * (__int128)(N - nle)) +
+                       CW * ((__int128)eta * (__int128)nle - sle);
+    const unsigned __int128 u = (unsigned __int128)S;  // S >= 0
+    cost[i] = __ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), (double)N);
+    cover[i] = nle;
+}
+
+hipError_t launch_moments(const int32_t *seg, const uint32_t *hist, int C, int64_t *count,
+                          int64_t *sum, int64_t *sumsq, int32_t *xmax, hipStream_t st)
+{
+    hipLaunchKernelGGL(moments_kernel, dim3(C), dim3(1024), 0, st, seg, hist, count, sum, sumsq,
+                       xmax);
+    return hipGetLastError();
+}
+
+hipError_t launch_reservation_cost(const int64_t *offsets, const int32_t *seg, const float *c_p,
+                                   const float *c_w, const uint32_t *hist, int S, int C, int R,
+                                   const int32_t *eta_r, uint32_t *cnt, uint64_t *sum,
+                                   double *cost, int64_t *cover, hipStream_t st)
+{
+    hipLaunchKernelGGL(prefix_kernel, dim3(S), dim3(1024), 0, st, hist, cnt, sum);
+    const long long n = (long long)R * C;
+    hipLaunchKernelGGL(reservation_cost_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                       st, offsets, seg, c_p, c_w, (const uint32_t *)cnt, (const uint64_t *)sum,
+                       C, n, eta_r, cost, cover);
     return hipGetLastError();
 }
 

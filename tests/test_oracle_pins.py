@@ -326,7 +326,7 @@ def test_fix_to_double_is_correctly_rounded():
 
 # ---------------------------------------------------------------- P13 ------
 # The block step: each class takes the exact best grid point that keeps every
-# group it is routed to within capacity (eq. capacity), given the others;
+# group it is routed to within capacity (the memory-capacity constraint of Sec. 3.4), given the others;
 # the sweep never increases the summed cost from a feasible start.
 
 def _feasible_kmax_exact(w, c, kcur):
@@ -426,3 +426,73 @@ def test_ties_lowest_multiplier():
             target = brute.saa_exact(int(w.eta[k]), xs, float(w.c_p[c]), float(w.c_w[c])) * len(xs)
             first = next(m for m in range(w.M) if F(S.as_int((c, k, m)), 1 << 33) == target)
             assert r["m_star"][0, c, k] == first
+
+
+# --------------------------------------------------------------- P15-P17 ---
+# Reservation cost (the per-arrival cost of Sec. 3.3 averaged over samples)
+# and per-class moments, used to price reservation policies against each other.
+
+@pytest.mark.parametrize("seed", range(5))
+def test_P15_reservation_cost_equals_rational_average(seed):
+    w = _tiny(200 + seed, C=3, N=(7, 1, 12), L=50)
+    rng = np.random.default_rng(seed)
+    eta = rng.integers(-5, 60, size=(6, w.C)).astype(np.int32)   # also below 0 and above L
+    cost, cover, S = oracle.reservation_cost(w, eta)
+    for r in range(eta.shape[0]):
+        for c in range(w.C):
+            xs = [int(v) for v in w.samples_of(c)]
+            cp, cw = float(w.c_p[c]), float(w.c_w[c])
+            want = brute.saa_exact(int(eta[r, c]), xs, cp, cw)
+            assert S.as_int((r, c)) == want * len(xs) * (1 << 33)
+            assert cost[r, c] == float(want * len(xs)) / len(xs)   # RN(RN(S) / N)
+            assert cover[r, c] == sum(1 for x in xs if x <= eta[r, c])
+
+
+def test_P15_closed_forms_at_the_ends():
+    w = _tiny(210, C=2, N=(40, 25), L=200)
+    m = oracle.moments(w)
+    top = int(w.L.max()) + 7
+    cost, cover, S = oracle.reservation_cost(w, np.array([[0, 0], [top, top]], np.int32))
+    for c in range(w.C):
+        n, s = int(m["count"][c]), int(m["sum"][c])
+        cp, cw = F(float(w.c_p[c])), F(float(w.c_w[c]))
+        assert F(S.as_int((0, c)), 1 << 33) == cp * s            # nothing reserved: all preempted
+        assert F(S.as_int((1, c)), 1 << 33) == cw * (top * n - s)  # above every sample: all waste
+        assert cover[0, c] == sum(1 for x in w.samples_of(c) if x <= 0) and cover[1, c] == n
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_P16_quantile_is_the_smallest_cost_minimiser(seed):
+    # Prop. 4.2 at eps = 0: the generalized-inverse quantile at c_p/(c_p+c_w)
+    # is the smallest integer reservation of least average cost.
+    w = _tiny(220 + seed, C=3, N=(31, 9, 57), L=90)
+    qv, _ = oracle.quantile(w)
+    L = int(w.L.max())
+    eta = np.repeat(np.arange(0, L + 1, dtype=np.int32)[:, None], w.C, axis=1)
+    _, _, S = oracle.reservation_cost(w, eta)
+    for c in range(w.C):
+        vals = [S.as_int((r, c)) for r in range(L + 1)]
+        best = min(vals)
+        assert vals.index(best) == qv[c]
+
+
+def test_P17_cost_slope_is_the_coverage_balance():
+    # S(eta + 1) - S(eta) = c_w #{x <= eta} - c_p #{x > eta}: ties the cost to cover.
+    w = _tiny(230, C=2, N=(33, 18), L=70)
+    eta = np.repeat(np.arange(-2, 74, dtype=np.int32)[:, None], w.C, axis=1)
+    _, cover, S = oracle.reservation_cost(w, eta)
+    for c in range(w.C):
+        n = w.n_of(c)
+        CP, CW = F(float(w.c_p[c])) * (1 << 33), F(float(w.c_w[c])) * (1 << 33)
+        for r in range(eta.shape[0] - 1):
+            d = S.as_int((r + 1, c)) - S.as_int((r, c))
+            assert d == CW * int(cover[r, c]) - CP * (n - int(cover[r, c]))
+
+
+def test_P17_moments_match_numpy():
+    w = random_workload(seed=240, C=3, N=(50, 1, 77), L=32768)
+    m = oracle.moments(w)
+    for c in range(w.C):
+        x = w.samples_of(c).astype(np.int64)
+        assert m["count"][c] == x.size and m["sum"][c] == x.sum()
+        assert m["sumsq"][c] == (x * x).sum() and m["xmax"][c] == x.max()

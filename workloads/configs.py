@@ -34,7 +34,7 @@ MAX_LEN = 1 << 15
 
 @dataclass
 class Groups:
-    """Serving-group capacity data for one block step (eq. capacity)."""
+    """Serving-group capacity data for one block step (the memory-capacity constraint of Sec. 3.4)."""
     cap: np.ndarray      # float32 [G]   KV capacity of each group, tokens
     conc: np.ndarray     # float32 [C*G] expected concurrent class-c requests on group g
     kappa: float         # safety factor (float32 value)
