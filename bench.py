@@ -1,7 +1,7 @@
 #!/usr/bin/env python3
 """Throughput of the DRO reservation path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload cfg3]
+    python bench.py [--steps K] [--warmup W] [--workload mixture-16x1M]
 
 One step is one pass of the whole hot path over the resident samples of the
 workload: the critical-fractile quantile of every class (class_quantile),
@@ -35,16 +35,16 @@ METRIC = "DRO cost evals/sec (class×r×λ×sample per s) + % fp32 VALU peak"
 VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 add/fma on MI355X
 
 # Hardware-counter figures of the dense kernel on the 16 x 1e6 workload, from
-# profiles/dense_kernel_cfg3_counters.md.  They describe one version of the
+# profiles/dense_kernel_mixture-16x1M_counters.md.  They describe one version of the
 # dense kernel's code (csrc/dense.hip and the constants of csrc/dro_internal.h,
 # comments and layout stripped, identified by the hash prefix) and are
 # reported as null for any other code or workload.
 DENSE_COUNTERS = {
     "dense_code_sha256_16": "adef0dc54cbbaa9b",
-    "workload": "cfg3",
+    "workload": "mixture-16x1M",
     "valu_instr_per_eval": 2.103,        # SQ_INSTS_VALU x 64 / evaluations
     "hbm_bytes_per_launch": 912119.9 * 1024,   # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
-    "source": "profiles/dense_kernel_cfg3_counters.md",
+    "source": "profiles/dense_kernel_mixture-16x1M_counters.md",
 }
 
 
@@ -98,7 +98,7 @@ def bench_bcd(ctx, dev, iters: int):
     import numpy as np
     import paper_2607_16892_amd as dro
     from workloads import make_workload
-    w = make_workload("cfg5", iteration=0)
+    w = make_workload("drift-8x4M", iteration=0)
     prob = dro.Problem.from_workload(w, dev)
     grp = dro.Groups.from_numpy(w.groups.cap, w.groups.conc, w.groups.kappa, dev)
     k = dro.bcd_init_state(ctx, prob)
@@ -106,7 +106,7 @@ def bench_bcd(ctx, dev, iters: int):
     binding = 0
     for it in range(iters):
         if it:
-            w = make_workload("cfg5", iteration=it)
+            w = make_workload("drift-8x4M", iteration=it)
             prob.replace_samples(w.offsets, w.xi)
         eps = torch.from_numpy(w.eps.copy()).to(dev)
         torch.cuda.synchronize()
@@ -121,7 +121,7 @@ def bench_bcd(ctx, dev, iters: int):
         binding = int((usage > 0.98 * w.groups.cap).sum())
     flags = ctx.take_flags()
     ms = float(np.median(times)) if times else None
-    return dict(workload="cfg5: 8 classes x 4e6 drifting lognormal, K=2048, M=256, G=6",
+    return dict(workload="drift-8x4M: 8 classes x 4e6 drifting lognormal, K=2048, M=256, G=6",
                 iters=iters, ms_per_iter=ms, evals_per_iter=w.evals,
                 evals_per_s=(w.evals / (ms / 1e3)) if ms else None,
                 binding_groups_last_iter=binding, flags=flags)
@@ -132,7 +132,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="cfg3")
+    ap.add_argument("--workload", default="mixture-16x1M")
     ap.add_argument("--cpu-samples", type=int, default=81920)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--bcd-iters", type=int, default=3)

@@ -1,6 +1,6 @@
 """Write the stored oracle results of the benchmark workloads.
 
-    python tests/golden/make_golden.py cfg1 cfg2 cfg3 cfg4 [cfg5:ITERS]
+    python tests/golden/make_golden.py lognormal-1x1k lognormal-4x100k mixture-16x1M ratios-8x250k [drift-8x4M:ITERS]
 
 Calls only `oracle/` (exact 128-bit evaluation, value-grouped) and the seeded
 generator in `workloads/`.  Each file records the generator checksum of its
@@ -46,7 +46,7 @@ def golden_bcd(iters: int) -> dict:
     rows = []
     k_prev = None
     for it in range(iters):
-        w = make_workload("cfg5", iteration=it)
+        w = make_workload("drift-8x4M", iteration=it)
         t0 = time.time()
         S = oracle.S_exact(w, grouped=True)
         W, _ = oracle.W_table(w, S)
@@ -60,17 +60,17 @@ def golden_bcd(iters: int) -> dict:
                          usage=[float(v).hex() for v in o["usage"]],
                          feasible=o["feasible"].tolist(), q_value=qv.tolist(),
                          seconds=round(time.time() - t0, 1)))
-        print(f"cfg5 iteration {it}: {rows[-1]['seconds']} s", flush=True)
+        print(f"drift-8x4M iteration {it}: {rows[-1]['seconds']} s", flush=True)
         k_prev = o["k_next"]
-    return dict(workload="cfg5", iterations=iters, k0=k0, rows=rows)
+    return dict(workload="drift-8x4M", iterations=iters, k0=k0, rows=rows)
 
 
 def main(argv):
     for arg in argv:
-        if arg.startswith("cfg5"):
+        if arg.startswith("drift-8x4M"):
             iters = int(arg.split(":")[1]) if ":" in arg else 50
             data = golden_bcd(iters)
-            path = os.path.join(HERE, "cfg5_bcd.json")
+            path = os.path.join(HERE, "drift-8x4M_bcd.json")
         else:
             data = golden_static(arg)
             path = os.path.join(HERE, f"{arg}.json")

@@ -23,7 +23,8 @@ def ctx(dev):
 def gpu_step(ctx, w, dev, k_prev=None):
     import torch
     import paper_2607_16892_amd as dro
-    print(f"[gpu] block step {w.name} C={w.C} K={w.K} M={w.M} G={w.groups.G}", flush=True)
+    print(f"[gpu] block step {w.name} iteration={w.meta.get('iteration') if w.meta else None} "
+          f"C={w.C} K={w.K} M={w.M} G={w.groups.G}", flush=True)
     prob = dro.Problem.from_workload(w, dev)
     eps = torch.from_numpy(w.eps[: w.C].copy()).to(dev)
     grp = dro.Groups.from_numpy(w.groups.cap, w.groups.conc, w.groups.kappa, dev)
@@ -68,14 +69,24 @@ def test_block_step_from_given_state(ctx, dev):
     assert np.array_equal(g["W_star"].view(np.uint64), o["W_star"].view(np.uint64))
 
 
-def test_cfg5_iterations_against_stored_oracle(ctx, dev):
-    path = os.path.join(HERE, "golden", "cfg5_bcd.json")
+def _drift_gold():
+    path = os.path.join(HERE, "golden", "drift-8x4M_bcd.json")
     if not os.path.exists(path):
         pytest.skip("no stored oracle results for the drifting block-step loop")
-    gold = json.load(open(path))
-    k_prev = None
-    for row in gold["rows"][:3]:
-        w = make_workload("cfg5", iteration=row["iteration"])
+    return json.load(open(path))
+
+
+@pytest.mark.parametrize("first", [0, 10, 20, 30, 40])
+def test_drift_iterations_against_stored_oracle(ctx, dev, first):
+    # 50 iterations of the drifting loop in chunks of 10; each chunk starts from
+    # the stored state entering its first iteration, then chains its own.
+    gold = _drift_gold()
+    rows = [r for r in gold["rows"] if first <= r["iteration"] < first + 10]
+    if not rows:
+        pytest.skip(f"the stored loop has no iteration {first}")
+    k_prev = None if first == 0 else np.array(rows[0]["k_prev"], np.int32)
+    for row in rows:
+        w = make_workload("drift-8x4M", iteration=row["iteration"])
         assert w.checksum() == row["checksum"]
         k0, g, flags = gpu_step(ctx, w, dev, k_prev)
         assert flags == 0
@@ -88,22 +99,22 @@ def test_cfg5_iterations_against_stored_oracle(ctx, dev):
         k_prev = g["k_next"]
 
 
-def _cfg5_tight(n=50_000, cap_scale=0.3):
+def _drift_tight(n=50_000, cap_scale=0.3):
     """The drifting 8-class workload's grid, costs and routing, the first n
     samples of each class, and capacities scaled down so that groups bind."""
     from workloads.configs import Workload, Groups
-    w = make_workload("cfg5", iteration=0)
+    w = make_workload("drift-8x4M", iteration=0)
     parts = [w.samples_of(c)[:n].copy() for c in range(w.C)]
     off = np.zeros(w.C + 1, np.int64)
     off[1:] = np.cumsum([len(p) for p in parts])
     g = Groups((w.groups.cap * np.float32(cap_scale)).astype(np.float32), w.groups.conc.copy(),
                w.groups.kappa)
-    return Workload("cfg5-tight", w.C, off, None, np.concatenate(parts), w.L, w.eta, w.lam,
+    return Workload("drift-8x4M-tight", w.C, off, None, np.concatenate(parts), w.L, w.eta, w.lam,
                     w.c_p, w.c_w, 1, w.eps.copy(), groups=g)
 
 
 def test_block_step_with_binding_capacity_at_full_grid(ctx, dev):
-    w = _cfg5_tight()
+    w = _drift_tight()
     k0, g, flags = gpu_step(ctx, w, dev)
     assert flags == 0
     S = oracle.S_exact(w)

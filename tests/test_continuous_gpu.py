@@ -61,10 +61,10 @@ def test_matches_exact_rational_dual(ctx, dev, seed):
     assert worst <= 1e-10
 
 
-def test_grid_and_saa_bounds_cfg2(ctx, dev):
+def test_grid_and_saa_bounds_lognormal_4x100k(ctx, dev):
     import torch
     import paper_2607_16892_amd as dro
-    w = make_workload("cfg2")
+    w = make_workload("lognormal-4x100k")
     W, g = run_cont(ctx, w, dev)
     prob = dro.Problem.from_workload(w, dev)
     ex = dro.dro_exact_table(ctx, prob, torch.from_numpy(w.eps).to(dev), want_argmin=False)
@@ -73,7 +73,7 @@ def test_grid_and_saa_bounds_cfg2(ctx, dev):
     # the grid is dense near gamma*: the two agree to a few 1e-3 at most
     assert np.max((Wg - W) / Wg) < 0.05
     # SAA lower bound, from the oracle with eps = 0 (the exact SAA table)
-    w0 = make_workload("cfg2")
+    w0 = make_workload("lognormal-4x100k")
     w0.eps[:] = 0
     saa, _ = oracle.W_table(w0, oracle.S_exact(w0))
     assert np.all(W >= saa * (1 - 1e-12))

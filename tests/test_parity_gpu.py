@@ -70,7 +70,7 @@ def check_against_oracle(w, g, kmax=None):
           f"W rel err {np.max(errW / np.maximum(ref['W'], 1e-300)):.2e}", flush=True)
 
 
-@pytest.mark.parametrize("name", ["cfg1", "cfg2"])
+@pytest.mark.parametrize("name", ["lognormal-1x1k", "lognormal-4x100k"])
 def test_full_config_against_oracle(ctx, dev, name):
     w = make_workload(name)
     check_against_oracle(w, run_gpu(ctx, w, dev))
@@ -102,7 +102,7 @@ def test_capacity_limited_argmin(ctx, dev):
 
 
 def test_deterministic_run_to_run(ctx, dev):
-    w = make_workload("cfg2")
+    w = make_workload("lognormal-4x100k")
     a, b = run_gpu(ctx, w, dev), run_gpu(ctx, w, dev)
     for k in ("S", "W", "m_star", "k_star", "W_star", "m_at_star", "q_value", "q_rank"):
         assert a[k].tobytes() == b[k].tobytes(), k
@@ -115,7 +115,7 @@ def _golden(name):
     return json.load(open(path))
 
 
-@pytest.mark.parametrize("name", ["cfg3", "cfg4"])
+@pytest.mark.parametrize("name", ["mixture-16x1M", "ratios-8x250k"])
 def test_large_config_against_stored_oracle(ctx, dev, name):
     gold = _golden(name)
     w = make_workload(name)
@@ -194,7 +194,7 @@ def check_exact_table(w, g, kmax=None):
     assert np.array_equal(g["m_at_star"], ref["m_at_star"])
 
 
-@pytest.mark.parametrize("name", ["cfg1", "cfg2"])
+@pytest.mark.parametrize("name", ["lognormal-1x1k", "lognormal-4x100k"])
 def test_exact_table_full_config(ctx, dev, name):
     w = make_workload(name)
     check_exact_table(w, run_exact_table(ctx, w, dev))
@@ -214,7 +214,7 @@ def test_exact_table_kink_and_capacity(ctx, dev):
     check_exact_table(w, run_exact_table(ctx, w, dev, k_max=kmax), kmax=kmax)
 
 
-@pytest.mark.parametrize("name", ["cfg3", "cfg4"])
+@pytest.mark.parametrize("name", ["mixture-16x1M", "ratios-8x250k"])
 def test_exact_table_large_config_against_stored_oracle(ctx, dev, name):
     gold = _golden(name)
     w = make_workload(name)

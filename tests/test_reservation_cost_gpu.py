@@ -71,7 +71,7 @@ def test_full_size_and_critical_fractile(ctx, dev):
     # critical-fractile quantile, where the cost is smallest (Prop. 4.2).
     import torch
     import paper_2607_16892_amd as dro
-    w = make_workload("cfg3")
+    w = make_workload("mixture-16x1M")
     prob = dro.Problem.from_workload(w, dev)
     q = dro.class_quantile(ctx, prob)["q_value"].cpu().numpy().astype(np.int64)
     offs = np.array([-50, -7, -1, 0, 1, 7, 50])

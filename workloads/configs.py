@@ -5,11 +5,11 @@ Sec. 5.1 "Experiment Setup") that are not available here.  The five workloads
 below are synthetic, seeded and heavy-tailed, with the class counts, sample
 counts, grid sizes, radii and cost ratios of the benchmark configurations:
 
-  cfg1  1 class  x 1,000      lognormal(5, 1), clip [1, 4096]       K=64   M=32
-  cfg2  4 classes x 100,000   lognormal, means 50/300/1500/600       K=512  M=128
-  cfg3  16 classes x 1e6      2-component lognormal mixture + Pareto K=2048 M=256
-  cfg4  8 segments x 250,000, 16 cost ratios x 16 radii              K=1024 M=128
-  cfg5  8 classes x 4e6, mean drifting 1 %/iteration, 6 groups       K=2048 M=256
+  lognormal-1x1k    1 class x 1,000       lognormal(5, 1), clip [1, 4096]         K=64   M=32
+  lognormal-4x100k  4 classes x 100,000   lognormal, means 50/300/1500/600         K=512  M=128
+  mixture-16x1M     16 classes x 1e6      2-component lognormal mixture + Lomax    K=2048 M=256
+  ratios-8x250k     8 segments x 250,000, 16 cost ratios x 16 radii                K=1024 M=128
+  drift-8x4M        8 classes x 4e6, mean drifting 1 %/iteration, 6 groups         K=2048 M=256
 
 Everything here is input generation: draws, rounding to integer lengths,
 the reservation and multiplier grids, radii as a fraction of the sample mean,
@@ -25,7 +25,8 @@ from typing import Optional
 
 import numpy as np
 
-CONFIG_NAMES = ("cfg1", "cfg2", "cfg3", "cfg4", "cfg5")
+CONFIG_NAMES = ("lognormal-1x1k", "lognormal-4x100k", "mixture-16x1M", "ratios-8x250k",
+                "drift-8x4M")
 
 # Sample lengths, grid points and support bounds are integers no larger than
 # 2**15; cost coefficients and multipliers lie in [2**-10, 2**7].
@@ -154,31 +155,31 @@ def _mean(x: np.ndarray) -> float:
 
 # -------------------------------------------------------------- configs ----
 
-def _cfg1() -> Workload:
+def _lognormal_1x1k() -> Workload:
     rng = np.random.default_rng(0)
     L = 4096
     x = _clip_round(rng.lognormal(5.0, 1.0, 1000), 1, L)
     offsets, xi = _csr([x])
-    return Workload("cfg1", 1, offsets, None, xi, np.array([L], np.int32),
+    return Workload("lognormal-1x1k", 1, offsets, None, xi, np.array([L], np.int32),
                     eta_grid(64, L), lam_grid(32), _f32([8.0]), _f32([1.0]),
                     1, _f32([10.0]),
                     meta=dict(desc="1 class x 1,000 lognormal(5,1) lengths, clip [1,4096]"))
 
 
-def _cfg2() -> Workload:
+def _lognormal_4x100k() -> Workload:
     rng = np.random.default_rng(1)
     L = 8192
     means, sig = (50.0, 300.0, 1500.0, 600.0), (0.8, 1.0, 1.2, 0.9)
     parts = [_clip_round(_lognormal_by_mean(rng, m, s, 100_000), 1, L) for m, s in zip(means, sig)]
     offsets, xi = _csr(parts)
     eps = _f32([0.05 * _mean(p) for p in parts])
-    return Workload("cfg2", 4, offsets, None, xi, np.full(4, L, np.int32),
+    return Workload("lognormal-4x100k", 4, offsets, None, xi, np.full(4, L, np.int32),
                     eta_grid(512, L), lam_grid(128), _f32([4, 8, 16, 32]), _f32([1] * 4),
                     1, eps,
                     meta=dict(desc="4 classes x 1e5 lognormal lengths, clip [1,8192]"))
 
 
-def _cfg3() -> Workload:
+def _mixture_16x1M() -> Workload:
     rng = np.random.default_rng(2)
     L, C, N = 32768, 16, 1_000_000
     parts, cps = [], []
@@ -195,14 +196,14 @@ def _cfg3() -> Workload:
         cps.append(math.exp(rng.uniform(math.log(2.0), math.log(64.0))))
     offsets, xi = _csr(parts)
     eps = _f32([0.02 * _mean(p) for p in parts])
-    return Workload("cfg3", C, offsets, None, xi, np.full(C, L, np.int32),
+    return Workload("mixture-16x1M", C, offsets, None, xi, np.full(C, L, np.int32),
                     eta_grid(2048, L), lam_grid(256), _f32(cps), _f32([1.0] * C),
                     1, eps,
                     meta=dict(desc="16 classes x 1e6: 0.7/0.3 lognormal mixture (means U[20,3000], "
                                    "sigma 1) + 2% Lomax(1.5) tail, clip [1,32768]"))
 
 
-def _cfg4() -> Workload:
+def _ratios_8x250k() -> Workload:
     """8 sample segments shared by 16 cost ratios: class c = ratio*8 + segment."""
     rng = np.random.default_rng(3)
     L, S, N, R, E = 32768, 8, 250_000, 16, 16
@@ -219,7 +220,7 @@ def _cfg4() -> Workload:
     for e in range(E):
         for c in range(C):
             eps[e * C + c] = np.float32(0.2 * smean[c % S] * e / 15.0)
-    return Workload("cfg4", C, offsets, seg, xi, np.full(C, L, np.int32),
+    return Workload("ratios-8x250k", C, offsets, seg, xi, np.full(C, L, np.int32),
                     eta_grid(1024, L), lam_grid(128), c_p, c_w, E, eps,
                     meta=dict(desc="8 segments x 2.5e5 lognormal (means 40..4000), "
                                    "x 16 ratios in [1,128] x 16 radii in [0, 0.2 mean]",
@@ -227,7 +228,7 @@ def _cfg4() -> Workload:
 
 
 @functools.lru_cache(maxsize=1)
-def _cfg5_base():
+def _drift_base():
     rng = np.random.default_rng(4)
     C, N, G = 8, 4_000_000, 6
     means = [40.0 * 100.0 ** (c / 7.0) for c in range(C)]
@@ -242,15 +243,15 @@ def _cfg5_base():
     return base, cps, cap, conc
 
 
-def _cfg5(iteration: int = 0) -> Workload:
-    base, cps, cap, conc = _cfg5_base()
+def _drift_8x4M(iteration: int = 0) -> Workload:
+    base, cps, cap, conc = _drift_base()
     L, C = 32768, 8
     drift = 1.01 ** iteration
     parts = [_clip_round(b * drift, 1, L) for b in base]
     offsets, xi = _csr(parts)
     eps = _f32([0.02 * _mean(p) for p in parts])
     groups = Groups(_f32(cap), _f32(conc.reshape(-1)), float(np.float32(0.2)))
-    return Workload("cfg5", C, offsets, None, xi, np.full(C, L, np.int32),
+    return Workload("drift-8x4M", C, offsets, None, xi, np.full(C, L, np.int32),
                     eta_grid(2048, L), lam_grid(256), _f32(cps), _f32([1.0] * C),
                     1, eps, groups=groups,
                     meta=dict(desc="8 classes x 4e6 lognormal (means 40..4000) drifting 1%/iteration; "
@@ -258,16 +259,16 @@ def _cfg5(iteration: int = 0) -> Workload:
 
 
 def make_workload(name: str, **kw) -> Workload:
-    if name == "cfg1":
-        return _cfg1()
-    if name == "cfg2":
-        return _cfg2()
-    if name == "cfg3":
-        return _cfg3()
-    if name == "cfg4":
-        return _cfg4()
-    if name == "cfg5":
-        return _cfg5(kw.get("iteration", 0))
+    if name == "lognormal-1x1k":
+        return _lognormal_1x1k()
+    if name == "lognormal-4x100k":
+        return _lognormal_4x100k()
+    if name == "mixture-16x1M":
+        return _mixture_16x1M()
+    if name == "ratios-8x250k":
+        return _ratios_8x250k()
+    if name == "drift-8x4M":
+        return _drift_8x4M(kw.get("iteration", 0))
     if name == "random":
         return random_workload(**kw)
     raise ValueError(f"unknown workload {name!r}")
