@@ -127,6 +127,56 @@ def bench_bcd(ctx, dev, iters: int):
                 binding_groups_last_iter=binding, flags=flags)
 
 
+def bench_policy(ctx, dev):
+    """Reservation policies priced on held-out and shifted samples (the
+    synthetic analogue of Tables 2 and 5, Fig. 2b and Fig. 3b)."""
+    import numpy as np
+    import torch
+    import paper_2607_16892_amd as dro
+    from paper_2607_16892_amd import policies
+    from workloads import policy_workloads
+    fr = [0.0, 0.05, 0.1, 0.15, 0.2, 0.3, 0.5]
+    tr, ev = policy_workloads(eps_fracs=fr)
+    train = dro.Problem.from_workload(tr, dev)
+    evalp = dro.Problem.from_workload(ev, dev)
+    eps = torch.from_numpy(tr.eps).to(dev)
+    policies.table(ctx, train, evalp, eps, fr)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    t = policies.table(ctx, train, evalp, eps, fr)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3
+    names = t["names"]
+    cost = t["cost"].cpu().numpy()                 # [R, shifts, rhos]
+    cov_tr = t["cover_train"].cpu().numpy()
+    rhos, shifts = tr.meta["rhos"], ev.meta["shifts"]
+    i = {n: names.index(n) for n in names}
+    dro_i = i["DRO(eps=0.15*mean)"]
+    n_tr = tr.n_of(0)
+
+    def r3(a):
+        return [float(f"{v:.4g}") for v in a]
+
+    return {
+        "workload": tr.meta["desc"] + f"; evaluation: {ev.meta['desc']}",
+        "ms_table": ms,
+        "rhos": rhos, "shifts": shifts,
+        "reservation": {n: t["eta"][i[n]].cpu().tolist() for n in names},
+        "cost_no_shift": {n: r3(cost[i[n], 0]) for n in names},
+        "dro_gain_vs_p90": r3(1.0 - cost[dro_i, 0] / cost[i["P90"], 0]),
+        "dro_gain_vs_p95": r3(1.0 - cost[dro_i, 0] / cost[i["P95"], 0]),
+        "dro_level_vs_qstar": {"level": r3(cov_tr[dro_i] / n_tr),
+                               "q_star": r3([r / (r + 1.0) for r in rhos])},
+        "saa_over_dro_by_shift": {str(s): r3(cost[i["SAA"], j] / cost[dro_i, j])
+                                  for j, s in enumerate(shifts)},
+        "dro_by_radius_at_largest_shift": {n: r3(cost[i[n], -1]) for n in names
+                                           if n.startswith("DRO")},
+        "note": "DRO at eps = 0.15 x mean (the paper's default); costs are the average "
+                "c_p (x - r)^+ + c_w (r - x)^+ over 1e6 held-out draws per shift, c_w = 1, "
+                "c_p = rho",
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,6 +186,8 @@ def main():
     ap.add_argument("--cpu-samples", type=int, default=81920)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--bcd-iters", type=int, default=3)
+    ap.add_argument("--no-policy", action="store_true",
+                    help="skip the reservation-policy comparison")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (scale reference for HBM byte counters)")
     args = ap.parse_args()
@@ -244,6 +296,10 @@ def main():
     if args.bcd_iters > 0:
         _log(f"block step, {args.bcd_iters} iterations")
         bcd = bench_bcd(ctx, dev, args.bcd_iters)
+    pol = None
+    if not args.no_policy:
+        _log("policy comparison")
+        pol = bench_policy(ctx, dev)
     cpu = None
     if not args.no_cpu_baseline:
         _log("cpu baseline (oracle)")
@@ -280,6 +336,7 @@ def main():
                      "counters": cnt["source"] if cnt else None},
         "cpu_baseline": cpu,
         "block_step": bcd,
+        "policy_comparison": pol,
         "continuous_dual": cont,
         "exact_table": {"ms": exact_ms, "same_optimum_as_dense_path": same_k and same_w,
                         "note": "dro_exact_table: the same W table from value counts and prefix "

@@ -1,6 +1,7 @@
 """Write the stored oracle results of the benchmark workloads.
 
-    python tests/golden/make_golden.py lognormal-1x1k lognormal-4x100k mixture-16x1M ratios-8x250k [drift-8x4M:ITERS]
+    python tests/golden/make_golden.py lognormal-1x1k lognormal-4x100k mixture-16x1M \
+        ratios-8x250k [drift-8x4M:ITERS] [policy-burst]
 
 Calls only `oracle/` (exact 128-bit evaluation, value-grouped) and the seeded
 generator in `workloads/`.  Each file records the generator checksum of its
@@ -65,9 +66,29 @@ def golden_bcd(iters: int) -> dict:
     return dict(workload="drift-8x4M", iterations=iters, k0=k0, rows=rows)
 
 
+def golden_policy() -> dict:
+    from oracle import policies
+    from workloads import policy_workloads
+    params = dict(trace="burst", n_train=1_000_000, n_eval=1_000_000,
+                  rhos=[2, 5, 10, 20, 50, 100], shifts=[1.0, 1.5, 2.0, 2.5, 3.0],
+                  eps_fracs=[0.0, 0.05, 0.1, 0.15, 0.2, 0.3, 0.5], L=8192, M=256, seed=5)
+    tr, ev = policy_workloads(**params)
+    t0 = time.time()
+    t = policies.table(tr, ev, params["eps_fracs"])
+    return dict(workload="policy-burst", params=params, checksum_train=tr.checksum(),
+                checksum_eval=ev.checksum(), oracle_seconds=round(time.time() - t0, 1),
+                names=t["names"], eta=t["eta"].tolist(), cover=t["cover"].tolist(),
+                cover_train=t["cover_train"].tolist(),
+                cost=[[[float(v).hex() for v in r] for r in rs] for rs in t["cost"]],
+                cost_train=[[float(v).hex() for v in r] for r in t["cost_train"]])
+
+
 def main(argv):
     for arg in argv:
-        if arg.startswith("drift-8x4M"):
+        if arg == "policy-burst":
+            data = golden_policy()
+            path = os.path.join(HERE, "policy-burst.json")
+        elif arg.startswith("drift-8x4M"):
             iters = int(arg.split(":")[1]) if ":" in arg else 50
             data = golden_bcd(iters)
             path = os.path.join(HERE, "drift-8x4M_bcd.json")

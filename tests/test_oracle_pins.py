@@ -496,3 +496,54 @@ def test_P17_moments_match_numpy():
         x = w.samples_of(c).astype(np.int64)
         assert m["count"][c] == x.size and m["sum"][c] == x.sum()
         assert m["sumsq"][c] == (x * x).sum() and m["xmax"][c] == x.max()
+
+
+# --------------------------------------------------------------- P18-P19 ---
+# The policy comparison (Sec. 5.1-5.4): baseline reservations by their plain
+# definitions, and the structure Prop. 4.2 puts on the table.
+
+def _policy_tiny(seed=0):
+    from workloads import policy_workloads
+    return policy_workloads(n_train=3000, n_eval=2000, rhos=(2, 10, 100), shifts=(1.0, 2.0),
+                            eps_fracs=(0.0, 0.15), L=600, K=601, M=48, seed=seed)
+
+
+def test_P18_baseline_reservations_by_definition():
+    from oracle import policies
+    tr, _ = _policy_tiny(1)
+    eta = policies.reservations(tr, (0.0, 0.15))
+    names = policies.policy_names((0.0, 0.15))
+    x = np.sort(tr.samples_of(0).astype(np.int64))
+    n = x.size
+    row = {nm: eta[i] for i, nm in enumerate(names)}
+    assert np.all(row["P90"] == x[(9 * n + 9) // 10 - 1])          # rank ceil(0.9 n)
+    assert np.all(row["P99"] == x[(99 * n + 99) // 100 - 1])
+    p95 = x[(19 * n + 19) // 20 - 1]
+    assert np.all(row["P95"] == ((p95 + 15) // 16) * 16)
+    assert np.all(row["Mean"] == -(-x.sum() // n))
+    assert np.all(row["Max"] == 600)
+    mu = x.mean()
+    sd = x.std()          # population standard deviation
+    for k in (1, 2):
+        r = row[f"LP+{k}sigma"][0]
+        assert r - 1 < mu + k * sd + 1e-9 and r >= mu + k * sd - 1e-9
+    # SAA is the critical-fractile quantile at rho/(rho+1) (Prop. 4.2)
+    for c, rho in enumerate((2, 10, 100)):
+        assert row["SAA"][c] == x[-(-rho * n // (rho + 1)) - 1]
+
+
+def test_P19_table_structure():
+    from oracle import policies
+    tr, ev = _policy_tiny(2)
+    t = policies.table(tr, ev, (0.0, 0.15))
+    names = t["names"]
+    i_dro0, i_saa, i_max = names.index("DRO(eps=0*mean)"), names.index("SAA"), names.index("Max")
+    # on an every-integer grid the eps = 0 DRO reservation is the SAA quantile
+    assert np.array_equal(t["eta"][i_dro0], t["eta"][i_saa])
+    # in sample, SAA has the least cost of all policies (Prop. 4.2)
+    assert np.all(t["cost_train"][i_saa][None, :] <= t["cost_train"])
+    # reserving L costs exactly c_w (L - mean) on every shifted set
+    for s in range(ev.C // tr.C):
+        xs = ev.samples_of(s * tr.C).astype(np.int64)
+        assert t["cost"][i_max, s, 0] == float(F(600 * xs.size - int(xs.sum()), xs.size))
+        assert np.all(t["cover"][i_max, s] == xs.size)

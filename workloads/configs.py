@@ -325,3 +325,78 @@ def random_workload(seed: int = 0, C: int = 3, N=(50, 7, 130), L: int = 300, K: 
     return Workload(f"random{seed}", C, offsets, seg, xi, np.full(C, L, np.int32),
                     eta_grid(K, L), lam_grid(M, lam_lo, lam_hi), c_p, c_w, E, eps,
                     groups=groups, meta=dict(desc=f"random seed={seed}"))
+
+
+# ------------------------------------------------- policy comparison ----
+# Lognormal stand-ins fitted to the summary statistics the paper prints for
+# its traces (Sec. 5.1): mean, P90 and P99 of the output length in tokens.
+TRACE_STATS = {
+    "burst": (125.0, 276.0, 1586.0),      # BurstGPT
+    "sharegpt": (265.0, 486.0, 768.0),    # ShareGPT
+}
+
+
+def fit_lognormal(mean: float, p90: float, p99: float) -> tuple[float, float]:
+    """(mu, sigma) of the lognormal with the given mean and P90.
+
+    mean = exp(mu + sigma^2 / 2) and P90 = exp(mu + z90 sigma) leave a
+    quadratic in sigma with two roots; the root whose P99 lies nearer the
+    printed P99 is taken.
+    """
+    from statistics import NormalDist
+    z90, z99 = NormalDist().inv_cdf(0.90), NormalDist().inv_cdf(0.99)
+    c = math.log(p90 / mean)
+    disc = z90 * z90 - 2.0 * c
+    if disc < 0:
+        raise ValueError("no lognormal has this mean and P90")
+    roots = (z90 - math.sqrt(disc), z90 + math.sqrt(disc))
+
+    def p99_err(s):
+        return abs(math.log(mean) - 0.5 * s * s + z99 * s - math.log(p99))
+
+    sigma = min(roots, key=p99_err)
+    return math.log(mean) - 0.5 * sigma * sigma, sigma
+
+
+def policy_workloads(trace: str = "burst", n_train: int = 1_000_000, n_eval: int = 1_000_000,
+                     rhos=(2, 5, 10, 20, 50, 100), shifts=(1.0, 1.5, 2.0, 2.5, 3.0),
+                     eps_fracs=(0.0, 0.05, 0.1, 0.15, 0.2, 0.3, 0.5), L: int = 8192,
+                     K: Optional[int] = None, M: int = 256, seed: int = 5):
+    """Training and evaluation sets for pricing reservation policies.
+
+    Training: n_train draws of one trace stand-in, rounded half-to-even and
+    clipped to [1, L], shared by one class per cost ratio rho (c_w = 1,
+    c_p = rho) through the segment map; radii eps = RN32(frac * sample mean)
+    for every frac in eps_fracs (row e of the radii).
+    Evaluation: for every shift factor s, n_eval fresh draws of the same
+    stand-in scaled by s before rounding and clipping (s is the ratio of the
+    evaluation mean to the training mean); class s * len(rhos) + i is
+    segment s priced at rho_i.  K defaults to every integer reservation
+    0..L.  Returns (train, eval) Workloads.
+    """
+    mu, sigma = fit_lognormal(*TRACE_STATS[trace])
+    rng = np.random.default_rng(seed)
+    x_train = _clip_round(rng.lognormal(mu, sigma, n_train), 1, L)
+    y_eval = rng.lognormal(mu, sigma, n_eval)
+    nr = len(rhos)
+    K = L + 1 if K is None else K
+    eta, lam = eta_grid(K, L), lam_grid(M)
+    mean = _mean(x_train)
+    eps = _f32([f * mean for f in eps_fracs for _ in range(nr)])
+    c_p, c_w = _f32(rhos), _f32([1.0] * nr)
+    off, xi = _csr([x_train])
+    desc = (f"{trace} stand-in lognormal(mu={mu:.4f}, sigma={sigma:.4f}), clip [1, {L}]: "
+            f"{n_train} training samples, {nr} cost ratios, {len(eps_fracs)} radii")
+    train = Workload(f"policy-{trace}-train", nr, off, np.zeros(nr, np.int32), xi,
+                     np.full(nr, L, np.int32), eta, lam, c_p, c_w, len(eps_fracs), eps,
+                     meta=dict(desc=desc, rhos=list(rhos), eps_fracs=list(eps_fracs)))
+    parts = [_clip_round(s * y_eval, 1, L) for s in shifts]
+    off_e, xi_e = _csr(parts)
+    ce = nr * len(shifts)
+    ev = Workload(f"policy-{trace}-eval", ce, off_e,
+                  np.array([c // nr for c in range(ce)], np.int32), xi_e,
+                  np.full(ce, L, np.int32), eta, lam, _f32([rhos[c % nr] for c in range(ce)]),
+                  _f32([1.0] * ce), 1, np.zeros(ce, np.float32),
+                  meta=dict(desc=f"{n_eval} fresh draws x shifts {list(shifts)}",
+                            shifts=list(shifts), rhos=list(rhos)))
+    return train, ev
