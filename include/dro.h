@@ -230,6 +230,126 @@ int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t
 int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const dro_groups *g,
                    const int32_t *k_prev, dro_step_out *out, dro_stream_t stream);
 
+/* ------------------------------------------------------------------------
+ * The rest of Alg. 1 (Sec. 4.3): the routing LP of Block 1 (LP1), prefix
+ * caching (Block 2) and the configuration search (Block 3), over the serving
+ * model of Sec. 3.1-3.4.  For class c and configuration g (z_g serving groups
+ * of tau_g x pp_g GPUs each):
+ *   T[c,g]    = pp_g alpha Lin_c / Cc_g + NL tau_g t_ar + beta E[xi_c] / Bc_g
+ *               (service time, Sec. 3.1, with E[xi_c] the class sample mean)
+ *   ET2[c,g]  = its second moment over the class samples
+ *   conc[c,g] = lam_c T_cg pi_cg / z_g   (concurrent requests, Little's law)
+ *   mem[g]    = (1 + kappa) (sum_c lam_c T_cg pi_cg (Lin_c + eta_c - delta_cg Lpre_c)) / z_g
+ *               + sum_c delta_cg Lpre_c   (KV tokens in use, the memory-capacity
+ *               constraint of Sec. 3.4 with r~ = r - delta L_pre, r = Lin + eta)
+ *   Wq[g]     = u (1 + Cs2) / (2 (1 - u)) Tbar, u = mem_g / Mcap_g: the
+ *               Pollaczek-Khinchin wait of Sec. 3.4 at the memory utilisation,
+ *               Tbar and Cs2 the mean and squared coefficient of variation of
+ *               the routed service times (Wq = 0 without traffic)
+ *   objective = sum_c lam_c (a_c W_c + sum_g pi_cg c_gpu tau_g pp_g T_cg + c_slo s_c
+ *               + (1 - a_c) c_rej), a_c = sum_g pi_cg,
+ *               s_c = max(0, sum_g pi_cg (Wq_g + T_cg) - a_c D_c)   (Prop. 4.1)
+ *   feasible  : sum_g z_g tau_g pp_g <= J; pi_cg > 0 only where z_g > 0;
+ *               mem_g <= u_max Mcap_g (1 + 1e-9) (u_max < 1 keeps the wait
+ *               finite; the slack keeps a routing that an LP left exactly at the
+ *               bound feasible).
+ * All double expressions are evaluated in a fixed order without contraction.
+ * Limits: 1 <= G <= 32, C * G <= 8192, 1 <= J <= 4096 and at most 2^32
+ * configurations in the search space, else DRO_ELIMIT.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int32_t G;                 /* candidate configurations */
+    const int32_t *tau, *pp;   /* device [G] tensor / pipeline degree (>= 1) */
+    const int32_t *tau_h, *pp_h; /* host copies of tau and pp */
+    const float *Mcap;         /* device [G] KV capacity of one group, tokens */
+    const float *Cc, *Bc;      /* device [G] prefill and decode rates, tokens/s */
+    const float *lam;          /* device [C] arrival rate, requests/s */
+    const int32_t *Lin, *Lpre; /* device [C] input length and cacheable prefix, tokens */
+    const float *D;            /* device [C] latency target, s */
+    float alpha, beta, t_ar;   /* prefill and decode constants, all-reduce latency (s) */
+    int32_t NL;                /* layers */
+    float c_gpu, c_slo, c_rej; /* cost per GPU-second, per second late, per rejection */
+    float kappa, u_max;        /* memory-headroom factor; utilisation bound in (0, 1) */
+    int32_t J;                 /* GPU budget */
+} dro_service;
+
+/* T and ET2 (device double [C*G], row c*G + g) from the exact class moments.
+ * Uses C, S, offsets, seg, xi, L of `p`. */
+int bcd_service_times(dro_ctx *ctx, const dro_problem *p, const dro_service *svc, double *T,
+                      double *ET2, dro_stream_t stream);
+
+/* Per configuration at a given state (all device arrays; pi, conc [C*G];
+ * z, Wq, cap, mem [G]; eta_c [C] = each class's reservation beyond its input;
+ * delta [C*G] 0/1): Wq, mem (may be NULL), conc, and
+ *   cap[g] = u_max Mcap_g - sum_c delta_cg Lpre_c
+ *            - (1 + kappa) (sum_c lam_c T_cg pi_cg (Lin_c - delta_cg Lpre_c)) / z_g,
+ * the memory left for the reservations (+inf where z_g = 0). */
+int bcd_queue_state(dro_ctx *ctx, int32_t C, const dro_service *svc, const double *T,
+                    const double *ET2, const double *pi, const int32_t *z, const int32_t *eta_c,
+                    const uint8_t *delta, double *Wq, double *cap, double *conc, double *mem,
+                    dro_stream_t stream);
+
+/* LP1 of Block 1: the routing pi >= 0 (device [C*G]) minimising the objective
+ * with the reservations, z and delta fixed and the wait Wq (device [G]) frozen
+ * at the incoming state, subject to sum_g pi_cg <= 1, the SLO slack rows and
+ * mem_g <= u_max Mcap_g.  Wc [C] holds each class's worst-case cost at its
+ * reservation.  Dense simplex with Bland's rule in one workgroup (fp64, rows
+ * scaled by their largest coefficient).  lp_objective (device double [1]) is
+ * the objective at the solution with s_c at its optimum; info (device int32
+ * [2]) = {pivots, status}: 0 optimal, 1 pivot limit, 2 infeasible at pi = 0
+ * (prefixes alone exceed a capacity), 3 unbounded. */
+int bcd_routing_lp(dro_ctx *ctx, int32_t C, const dro_service *svc, const double *Wc,
+                   const double *T, const double *Wq, const int32_t *z, const int32_t *eta_c,
+                   const uint8_t *delta, double *pi, double *lp_objective, int32_t *info,
+                   dro_stream_t stream);
+
+/* LP2 of Block 1 on the grid: one Gauss-Seidel sweep over c = 0..C-1 of the
+ * exact table W (device double [C*K]): with the other classes at their
+ * current grid points, bound_g = (cap_g - (1+kappa) sum_{c' != c} conc_c'g
+ * eta[k_c']) / ((1+kappa) conc_cg) over the g with conc_cg > 0, kmax = the
+ * largest k with eta[k] <= min_g bound_g + 1e-6 (none: kmax = 0,
+ * feasible[c] = 0),
+ * k_out[c] = the lowest argmin of W[c, 0..kmax].  feasible may be NULL. */
+int bcd_reservation_sweep(dro_ctx *ctx, int32_t C, int32_t K, const double *W,
+                          const int32_t *eta, int32_t G, const double *conc, const double *cap,
+                          float kappa, const int32_t *k_in, int32_t *k_out, uint8_t *feasible,
+                          dro_stream_t stream);
+
+/* Block 2: delta[c*G + g] = 1[conc_cg > 1] (device arrays). */
+int bcd_prefix_cache(dro_ctx *ctx, int32_t C, int32_t G, const double *conc, uint8_t *delta,
+                     dro_stream_t stream);
+
+/* Block 3: every z in Z = {z >= 0 : sum_g z_g tau_g pp_g <= J}, one thread
+ * per z in lexicographic order of (z_0, .., z_{G-1}), evaluated with pi, the
+ * reservations and delta fixed; the first minimiser of the objective over the
+ * feasible z replaces z (device int32 [G], in/out) unless the incoming z
+ * attains the minimum (no feasible z: z is kept).  best_objective (double),
+ * best_rank and n_feasible (int64) are device scalars (rank -1: none). */
+int bcd_config_search(dro_ctx *ctx, int32_t C, const dro_service *svc, const double *Wc,
+                      const double *T, const double *ET2, const double *pi,
+                      const int32_t *eta_c, const uint8_t *delta, int32_t *z,
+                      double *best_objective, int64_t *best_rank, int64_t *n_feasible,
+                      dro_stream_t stream);
+
+/* Alg. 1 with the reservation on the grid.  Start: z (device int32 [G], in),
+ * delta = 0, pi = 0, reservations at the largest grid point not above the
+ * class mean (Alg. 1 init); the worst-case table W[c,k] of radius row eps[C]
+ * is computed once, exactly (as dro_exact_table).  Block 1 takes the wait Wq
+ * at the state entering it and alternates bcd_routing_lp (with that Wq) and
+ * bcd_reservation_sweep until the reservations repeat and max |pi change|
+ * <= 1e-9, at most max_inner times; Block 2 sets delta; Block 3 runs bcd_config_search; the
+ * loop ends when z and delta repeat, after at most max_outer iterations.
+ * Outputs (device): z [G], k [C], pi [C*G], delta [C*G], objective [1] (at
+ * the final state).  info (host int32 [4]) = {outer iterations, Block 1
+ * rounds, simplex pivots, status bits: 1 pivot limit, 2 infeasible LP start,
+ * 4 unbounded LP, 8 a class without a feasible reservation, 16 Block 1 hit
+ * max_inner, 32 the loop hit max_outer}.  Synchronises the stream once per
+ * Block 1 round (the loop's decisions are read on the host).  Uses every
+ * field of `p`. */
+int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dro_service *svc,
+                  int32_t max_outer, int32_t max_inner, int32_t *z, int32_t *k, double *pi,
+                  uint8_t *delta, double *objective, int32_t *info, dro_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

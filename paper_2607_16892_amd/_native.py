@@ -25,6 +25,14 @@ class GroupsStruct(ct.Structure):
     _fields_ = [("G", i32), ("cap", P), ("conc", P), ("kappa", ct.c_float)]
 
 
+class ServiceStruct(ct.Structure):
+    _fields_ = [("G", i32), ("tau", P), ("pp", P), ("tau_h", P), ("pp_h", P), ("Mcap", P),
+                ("Cc", P), ("Bc", P), ("lam", P), ("Lin", P), ("Lpre", P), ("D", P),
+                ("alpha", ct.c_float), ("beta", ct.c_float), ("t_ar", ct.c_float), ("NL", i32),
+                ("c_gpu", ct.c_float), ("c_slo", ct.c_float), ("c_rej", ct.c_float),
+                ("kappa", ct.c_float), ("u_max", ct.c_float), ("J", i32)]
+
+
 class StepOutStruct(ct.Structure):
     _fields_ = [("k_next", P), ("W_star", P), ("q_value", P), ("usage", P), ("feasible", P)]
 
@@ -44,6 +52,18 @@ EXPORTS = {
     "class_moments": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P, P, P, P]),
     "dro_reservation_cost": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P]),
     "bcd_init_state": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P]),
+    "bcd_service_times": (ct.c_int, [P, ct.POINTER(ProblemStruct), ct.POINTER(ServiceStruct), P, P,
+                                     P]),
+    "bcd_queue_state": (ct.c_int, [P, i32, ct.POINTER(ServiceStruct), P, P, P, P, P, P, P, P, P,
+                                   P, P]),
+    "bcd_routing_lp": (ct.c_int, [P, i32, ct.POINTER(ServiceStruct), P, P, P, P, P, P, P, P, P,
+                                  P]),
+    "bcd_reservation_sweep": (ct.c_int, [P, i32, i32, P, P, i32, P, P, ct.c_float, P, P, P, P]),
+    "bcd_prefix_cache": (ct.c_int, [P, i32, i32, P, P, P]),
+    "bcd_config_search": (ct.c_int, [P, i32, ct.POINTER(ServiceStruct), P, P, P, P, P, P, P, P, P,
+                                     P, P]),
+    "dro_bcd_solve": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, ct.POINTER(ServiceStruct), i32,
+                                 i32, P, P, P, P, P, P, P]),
     "bcd_block_step": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, ct.POINTER(GroupsStruct), P,
                                   ct.POINTER(StepOutStruct), P]),
 }

@@ -28,6 +28,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
 UNITS = {
     "dense.hip": [],
     "exact.hip": ["-ffp-contract=off"],
+    "serving.hip": ["-ffp-contract=off"],
     "api.hip": ["-ffp-contract=off"],
 }
 

@@ -18,6 +18,10 @@ struct dro_ctx {
     size_t ws_size = 0;
     uint32_t *flags = nullptr;  // device word of DRO_FLAG_* bits
     char err[1024] = {0};
+    // host staging of the configuration-space count table (kept alive until
+    // the next configuration search on this context has been enqueued)
+    std::vector<long long> ways_h;
+    std::vector<int32_t> gpus_h;
 };
 
 namespace {
@@ -749,6 +753,393 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     }
     HIPCHK(launch_bcd_finish(p->eta, C, p->K, grp->G, grp->conc, grp->kappa, kcur, out->usage,
                              out->k_next, st));
+    return DRO_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------------
+// Serving model: routing LP, prefix caching, configuration search, Alg. 1.
+// ------------------------------------------------------------------------
+namespace {
+
+constexpr int kMaxServiceG = 32;
+constexpr long long kMaxConfigs = 1LL << 32;
+constexpr double kPiTol = 1e-9;
+
+int check_service(dro_ctx *ctx, int C, const dro_service *v)
+{
+    if (!ctx) return DRO_EINVAL;
+    if (!v) return fail(ctx, DRO_EINVAL, "service is NULL");
+    if (C <= 0) return fail(ctx, DRO_EINVAL, "C must be positive (C=%d)", C);
+    if (v->G <= 0) return fail(ctx, DRO_EINVAL, "G must be positive (G=%d)", v->G);
+    if (v->G > kMaxServiceG)
+        return fail(ctx, DRO_ELIMIT, "G=%d exceeds %d configurations", v->G, kMaxServiceG);
+    if ((long long)C * v->G > 8192)
+        return fail(ctx, DRO_ELIMIT, "C*G=%lld exceeds 8192 routing variables", (long long)C * v->G);
+    if (!v->tau || !v->pp || !v->tau_h || !v->pp_h || !v->Mcap || !v->Cc || !v->Bc || !v->lam ||
+        !v->Lin || !v->Lpre || !v->D)
+        return fail(ctx, DRO_EINVAL, "a required array of the service model is NULL");
+    if (v->J <= 0 || v->J > 4096) return fail(ctx, DRO_ELIMIT, "J=%d outside [1, 4096]", v->J);
+    const float sc[] = {v->alpha, v->beta, v->t_ar, v->c_gpu, v->c_slo, v->c_rej, v->kappa};
+    for (float x : sc)
+        if (!std::isfinite(x) || x < 0.0f)
+            return fail(ctx, DRO_EINVAL, "service constants must be finite and >= 0");
+    if (!(v->u_max > 0.0f && v->u_max < 1.0f))
+        return fail(ctx, DRO_EINVAL, "u_max=%g must lie in (0, 1)", (double)v->u_max);
+    if (v->NL < 0) return fail(ctx, DRO_EINVAL, "NL must be >= 0");
+    for (int g = 0; g < v->G; ++g)
+        if (v->tau_h[g] < 1 || v->pp_h[g] < 1 || (long long)v->tau_h[g] * v->pp_h[g] > 4096)
+            return fail(ctx, DRO_EINVAL, "configuration %d: tau=%d pp=%d", g, v->tau_h[g], v->pp_h[g]);
+    return DRO_OK;
+}
+
+SvcArgs svc_args(const dro_service *v, int C)
+{
+    SvcArgs s;
+    s.C = C;
+    s.G = v->G;
+    s.tau = v->tau;
+    s.pp = v->pp;
+    s.Mcap = v->Mcap;
+    s.Cc = v->Cc;
+    s.Bc = v->Bc;
+    s.lam = v->lam;
+    s.Lin = v->Lin;
+    s.Lpre = v->Lpre;
+    s.D = v->D;
+    s.alpha = v->alpha;
+    s.beta = v->beta;
+    s.t_ar = v->t_ar;
+    s.NL = (double)v->NL;
+    s.c_gpu = v->c_gpu;
+    s.c_slo = v->c_slo;
+    s.c_rej = v->c_rej;
+    s.kappa = v->kappa;
+    s.u_max = v->u_max;
+    s.J = v->J;
+    return s;
+}
+
+// ways[g][b] = number of (z_g, .., z_{G-1}) >= 0 with sum z_h gpus_h <= b,
+// saturating; fills ctx->ways_h and ctx->gpus_h and returns |Z| (or -1).
+long long count_configs(dro_ctx *ctx, const dro_service *v, hipStream_t st)
+{
+    // an earlier search may still be copying the previous table
+    if (!ctx->ways_h.empty() && hipStreamSynchronize(st) != hipSuccess) return -1;
+    const int G = v->G, J = v->J;
+    ctx->gpus_h.assign(G, 0);
+    for (int g = 0; g < G; ++g) ctx->gpus_h[g] = v->tau_h[g] * v->pp_h[g];
+    std::vector<long long> &w = ctx->ways_h;
+    w.assign((size_t)(G + 1) * (J + 1), 0);
+    const long long cap = 1LL << 62;
+    for (int b = 0; b <= J; ++b) w[(size_t)G * (J + 1) + b] = 1;
+    for (int g = G - 1; g >= 0; --g)
+        for (int b = 0; b <= J; ++b) {
+            long long acc = 0;
+            for (int u = 0; u * ctx->gpus_h[g] <= b; ++u) {
+                acc += w[(size_t)(g + 1) * (J + 1) + (b - u * ctx->gpus_h[g])];
+                if (acc > cap) acc = cap;
+            }
+            w[(size_t)g * (J + 1) + b] = acc;
+        }
+    return w[J];
+}
+
+size_t config_bytes(int C, int G, int J, long long nz)
+{
+    const long long nb = (nz + 255) / 256;
+    return rup(config_pre_doubles(C, G) * 8) + rup((size_t)G * 4) + rup((size_t)(G + 1) * (J + 1) * 8) +
+           rup((size_t)G * 4) + rup((size_t)nb * 8) * 3 + 3 * rup(8) + rup(4 * 8);
+}
+
+struct ConfigBufs {
+    double *pre_d;
+    int32_t *route, *gpus;
+    long long *ways;
+    double *part_obj;
+    long long *part_rank, *part_feas;
+    double *best_obj;
+    long long *best_rank, *n_feas;
+    int32_t *flag;
+};
+
+ConfigBufs take_config(Arena &ar, int C, int G, int J, long long nz)
+{
+    const long long nb = (nz + 255) / 256;
+    ConfigBufs b;
+    b.pre_d = ar.take<double>(config_pre_doubles(C, G));
+    b.route = ar.take<int32_t>(G);
+    b.ways = ar.take<long long>((size_t)(G + 1) * (J + 1));
+    b.gpus = ar.take<int32_t>(G);
+    b.part_obj = ar.take<double>(nb);
+    b.part_rank = ar.take<long long>(nb);
+    b.part_feas = ar.take<long long>(nb);
+    b.best_obj = ar.take<double>(1);
+    b.best_rank = ar.take<long long>(1);
+    b.n_feas = ar.take<long long>(1);
+    b.flag = ar.take<int32_t>(8);
+    return b;
+}
+
+int upload_configs(dro_ctx *ctx, const ConfigBufs &b, int G, int J, hipStream_t st)
+{
+    HIPCHK(hipMemcpyAsync(b.ways, ctx->ways_h.data(), sizeof(long long) * (size_t)(G + 1) * (J + 1),
+                          hipMemcpyHostToDevice, st));
+    HIPCHK(hipMemcpyAsync(b.gpus, ctx->gpus_h.data(), sizeof(int32_t) * G, hipMemcpyHostToDevice, st));
+    return DRO_OK;
+}
+
+int max_pivots(int C, int G) { return 50 * (3 * C + G + C * G) + 1000; }
+
+}  // namespace
+
+extern "C" {
+
+int bcd_service_times(dro_ctx *ctx, const dro_problem *p, const dro_service *svc, double *T,
+                      double *ET2, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
+    if (rc) return rc;
+    rc = check_service(ctx, p->C, svc);
+    if (rc) return rc;
+    if (!T || !ET2) return fail(ctx, DRO_EINVAL, "T and ET2 must be non-NULL");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const int C = p->C;
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + 4 * rup((size_t)C * 8), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    int64_t *cnt = ar.take<int64_t>(C), *sum = ar.take<int64_t>(C), *ssq = ar.take<int64_t>(C);
+    int32_t *xmax = ar.take<int32_t>(C);
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_moments(p->seg, qb.hist, C, cnt, sum, ssq, xmax, st));
+    HIPCHK(launch_service_times(svc_args(svc, C), cnt, sum, ssq, T, ET2, st));
+    return DRO_OK;
+}
+
+int bcd_queue_state(dro_ctx *ctx, int32_t C, const dro_service *svc, const double *T,
+                    const double *ET2, const double *pi, const int32_t *z, const int32_t *eta_c,
+                    const uint8_t *delta, double *Wq, double *cap, double *conc, double *mem,
+                    dro_stream_t stream)
+{
+    int rc = check_service(ctx, C, svc);
+    if (rc) return rc;
+    if (!T || !ET2 || !pi || !z || !eta_c || !delta || !Wq || !cap || !conc)
+        return fail(ctx, DRO_EINVAL, "a queue-state argument is NULL");
+    DeviceGuard g(ctx->device);
+    HIPCHK(launch_state(svc_args(svc, C), T, ET2, pi, z, eta_c, delta, Wq, cap, conc, mem,
+                        (hipStream_t)stream));
+    return DRO_OK;
+}
+
+int bcd_routing_lp(dro_ctx *ctx, int32_t C, const dro_service *svc, const double *Wc,
+                   const double *T, const double *Wq, const int32_t *z, const int32_t *eta_c,
+                   const uint8_t *delta, double *pi, double *lp_objective, int32_t *info,
+                   dro_stream_t stream)
+{
+    int rc = check_service(ctx, C, svc);
+    if (rc) return rc;
+    if (!Wc || !T || !Wq || !z || !eta_c || !delta || !pi || !lp_objective || !info)
+        return fail(ctx, DRO_EINVAL, "a routing-LP argument is NULL");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const int G = svc->G, m = 2 * C + G;
+    rc = ensure_ws(ctx, rup(lp1_tableau_doubles(C, G) * 8) + rup((size_t)m * 4), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    double *work = ar.take<double>(lp1_tableau_doubles(C, G));
+    int32_t *basis = ar.take<int32_t>(m);
+    HIPCHK(launch_lp1(svc_args(svc, C), Wc, T, Wq, z, eta_c, delta, work, basis, max_pivots(C, G),
+                      pi, lp_objective, info, st));
+    return DRO_OK;
+}
+
+int bcd_reservation_sweep(dro_ctx *ctx, int32_t C, int32_t K, const double *W,
+                          const int32_t *eta, int32_t G, const double *conc, const double *cap,
+                          float kappa, const int32_t *k_in, int32_t *k_out, uint8_t *feasible,
+                          dro_stream_t stream)
+{
+    if (!ctx) return DRO_EINVAL;
+    if (C <= 0 || K <= 0 || G <= 0 || !W || !eta || !conc || !cap || !k_in || !k_out)
+        return fail(ctx, DRO_EINVAL, "sweep needs C, K, G > 0 and non-NULL W, eta, conc, cap, k");
+    if (!std::isfinite(kappa) || kappa < 0.0f) return fail(ctx, DRO_EINVAL, "kappa must be >= 0");
+    if (k_in == k_out) return fail(ctx, DRO_EINVAL, "k_in and k_out must differ");
+    DeviceGuard g(ctx->device);
+    HIPCHK(launch_sweep(W, eta, C, K, G, conc, cap, kappa, k_in, k_out, feasible,
+                        (hipStream_t)stream));
+    return DRO_OK;
+}
+
+int bcd_prefix_cache(dro_ctx *ctx, int32_t C, int32_t G, const double *conc, uint8_t *delta,
+                     dro_stream_t stream)
+{
+    if (!ctx) return DRO_EINVAL;
+    if (C <= 0 || G <= 0 || !conc || !delta)
+        return fail(ctx, DRO_EINVAL, "prefix cache needs C, G > 0 and non-NULL conc, delta");
+    DeviceGuard g(ctx->device);
+    HIPCHK(launch_cache(conc, C * G, delta, (hipStream_t)stream));
+    return DRO_OK;
+}
+
+int bcd_config_search(dro_ctx *ctx, int32_t C, const dro_service *svc, const double *Wc,
+                      const double *T, const double *ET2, const double *pi,
+                      const int32_t *eta_c, const uint8_t *delta, int32_t *z,
+                      double *best_objective, int64_t *best_rank, int64_t *n_feasible,
+                      dro_stream_t stream)
+{
+    int rc = check_service(ctx, C, svc);
+    if (rc) return rc;
+    if (!Wc || !T || !ET2 || !pi || !eta_c || !delta || !z)
+        return fail(ctx, DRO_EINVAL, "a configuration-search argument is NULL");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const long long nz = count_configs(ctx, svc, st);
+    if (nz < 0) return fail(ctx, DRO_EHIP, "stream synchronisation failed");
+    if (nz > kMaxConfigs)
+        return fail(ctx, DRO_ELIMIT, "%lld configurations exceed 2^32", nz);
+    const int G = svc->G, J = svc->J;
+    rc = ensure_ws(ctx, config_bytes(C, G, J, nz), st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    const ConfigBufs b = take_config(ar, C, G, J, nz);
+    rc = upload_configs(ctx, b, G, J, st);
+    if (rc) return rc;
+    HIPCHK(launch_config_search(svc_args(svc, C), nz, b.gpus, b.ways, Wc, T, ET2, pi, eta_c, delta,
+                                b.pre_d, b.route, b.part_obj, b.part_rank, b.part_feas, z, nullptr,
+                                nullptr, best_objective ? best_objective : b.best_obj,
+                                best_rank ? (long long *)best_rank : b.best_rank,
+                                n_feasible ? (long long *)n_feasible : b.n_feas, b.flag, st));
+    return DRO_OK;
+}
+
+int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dro_service *svc,
+                  int32_t max_outer, int32_t max_inner, int32_t *z, int32_t *k, double *pi,
+                  uint8_t *delta, double *objective, int32_t *info, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
+    if (rc) return rc;
+    rc = check_service(ctx, p->C, svc);
+    if (rc) return rc;
+    if (!eps || !z || !k || !pi || !delta || !objective || !info)
+        return fail(ctx, DRO_EINVAL, "a solver argument is NULL");
+    if (max_outer <= 0 || max_inner <= 0)
+        return fail(ctx, DRO_EINVAL, "max_outer and max_inner must be positive");
+    DeviceGuard g(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    const int C = p->C, G = svc->G, K = p->K, J = svc->J, CG = C * G, m = 2 * C + G;
+    const long long nz = count_configs(ctx, svc, st);
+    if (nz < 0) return fail(ctx, DRO_EHIP, "stream synchronisation failed");
+    if (nz > kMaxConfigs) return fail(ctx, DRO_ELIMIT, "%lld configurations exceed 2^32", nz);
+    const size_t bins = (size_t)p->S * kHistBins;
+    const size_t need = stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) +
+                        rup(bins * 8) + rup((size_t)C * K * 8) + rup((size_t)C * K * 4) +
+                        4 * rup((size_t)C * 8) + rup(lp1_tableau_doubles(C, G) * 8) +
+                        rup((size_t)m * 4) + 4 * rup((size_t)CG * 8) + 2 * rup((size_t)CG) +
+                        7 * rup((size_t)G * 8) + 6 * rup((size_t)C * 8) +
+                        config_bytes(C, G, J, nz) + rup(64);
+    rc = ensure_ws(ctx, need, st);
+    if (rc) return rc;
+    Arena ar{(char *)ctx->ws, 0};
+    dro_problem q;
+    rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
+    const SvcArgs s = svc_args(svc, C);
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    uint32_t *pcnt = ar.take<uint32_t>(bins);
+    uint64_t *psum = ar.take<uint64_t>(bins);
+    double *W = ar.take<double>((size_t)C * K);
+    int32_t *mstar = ar.take<int32_t>((size_t)C * K);
+    int64_t *cnt = ar.take<int64_t>(C), *sum = ar.take<int64_t>(C), *ssq = ar.take<int64_t>(C);
+    int32_t *xmax = ar.take<int32_t>(C);
+    double *work = ar.take<double>(lp1_tableau_doubles(C, G));
+    int32_t *basis = ar.take<int32_t>(m);
+    double *T = ar.take<double>(CG), *ET2 = ar.take<double>(CG), *pi_new = ar.take<double>(CG);
+    double *conc = ar.take<double>(CG);
+    uint8_t *d_new = ar.take<uint8_t>(CG), *feas = ar.take<uint8_t>(C);
+    double *Wq = ar.take<double>(G), *cap = ar.take<double>(G), *lpobj = ar.take<double>(1);
+    double *Wq_blk = ar.take<double>(G);
+    double *Wc = ar.take<double>(C);
+    int32_t *eta_c = ar.take<int32_t>(C), *k_new = ar.take<int32_t>(C);
+    unsigned long long *sums = ar.take<unsigned long long>(C);
+    int32_t *ctl = ar.take<int32_t>(8);  // converge flag, lp pivots, lp status
+    const ConfigBufs cb = take_config(ar, C, G, J, nz);
+    rc = upload_configs(ctx, cb, G, J, st);
+    if (rc) return rc;
+
+    // the exact worst-case table of the radius row, the moments, the service times, r0
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, nullptr,
+                              qb.hist, p->S, 1, C, K, p->M, pcnt, psum, W, mstar, nullptr, nullptr,
+                              nullptr, st));
+    HIPCHK(launch_moments(p->seg, qb.hist, C, cnt, sum, ssq, xmax, st));
+    HIPCHK(launch_service_times(s, cnt, sum, ssq, T, ET2, st));
+    HIPCHK(launch_bcd_init(p->offsets, p->seg, p->xi, p->eta, C, K, sh.max_n, sums, k, st));
+    HIPCHK(launch_fill_u32(reinterpret_cast<uint32_t *>(pi), 2LL * CG, 0u, st));
+    HIPCHK(launch_zero_u8(delta, CG, st));
+
+    int outer = 0, inner = 0, pivots = 0, status = 0;
+    const int mp = max_pivots(C, G);
+    for (int it = 0; it < max_outer; ++it) {
+        ++outer;
+        bool converged = false;
+        // the wait is linearised once per Block 1, at the state entering it
+        HIPCHK(launch_gather(W, p->eta, k, C, K, Wc, eta_c, st));
+        HIPCHK(launch_state(s, T, ET2, pi, z, eta_c, delta, Wq_blk, cap, conc, nullptr, st));
+        for (int jt = 0; jt < max_inner; ++jt) {
+            ++inner;
+            HIPCHK(launch_gather(W, p->eta, k, C, K, Wc, eta_c, st));
+            HIPCHK(launch_lp1(s, Wc, T, Wq_blk, z, eta_c, delta, work, basis, mp, pi_new, lpobj,
+                              ctl + 1, st));
+            HIPCHK(launch_state(s, T, ET2, pi_new, z, eta_c, delta, Wq, cap, conc, nullptr, st));
+            HIPCHK(launch_sweep(W, p->eta, C, K, G, conc, cap, svc->kappa, k, k_new, feas, st));
+            HIPCHK(launch_converge(C, G, kPiTol, k_new, k, pi_new, pi, ctl, st));
+            int32_t h[3];
+            HIPCHK(hipMemcpyAsync(h, ctl, sizeof(h), hipMemcpyDeviceToHost, st));
+            HIPCHK(hipStreamSynchronize(st));
+            pivots += h[1];
+            if (h[2] == 1) status |= 1;
+            if (h[2] == 2) status |= 2;
+            if (h[2] == 3) status |= 4;
+            if (h[0]) {
+                converged = true;
+                break;
+            }
+        }
+        if (!converged) status |= 16;
+        // Block 2, then Block 3 with the new delta
+        HIPCHK(launch_gather(W, p->eta, k, C, K, Wc, eta_c, st));
+        HIPCHK(launch_state(s, T, ET2, pi, z, eta_c, delta, Wq, cap, conc, nullptr, st));
+        HIPCHK(launch_cache(conc, CG, d_new, st));
+        HIPCHK(launch_config_search(s, nz, cb.gpus, cb.ways, Wc, T, ET2, pi, eta_c, d_new, cb.pre_d,
+                                    cb.route, cb.part_obj, cb.part_rank, cb.part_feas, z, d_new,
+                                    delta, cb.best_obj, cb.best_rank, cb.n_feas, cb.flag, st));
+        int32_t changed = 0;
+        HIPCHK(hipMemcpyAsync(&changed, cb.flag, sizeof(changed), hipMemcpyDeviceToHost, st));
+        HIPCHK(hipStreamSynchronize(st));
+        if (!changed) break;
+        if (it == max_outer - 1) status |= 32;
+    }
+    HIPCHK(launch_gather(W, p->eta, k, C, K, Wc, eta_c, st));
+    HIPCHK(launch_state_objective(s, T, ET2, pi, z, eta_c, delta, Wc, cb.pre_d, cb.route,
+                                  objective, st));
+    std::vector<uint8_t> fh(C);
+    HIPCHK(hipMemcpyAsync(fh.data(), feas, C, hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    for (int c = 0; c < C; ++c)
+        if (!fh[c]) status |= 8;
+    info[0] = outer;
+    info[1] = inner;
+    info[2] = pivots;
+    info[3] = status;
     return DRO_OK;
 }
 

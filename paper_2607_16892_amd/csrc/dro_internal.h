@@ -160,6 +160,53 @@ hipError_t launch_bcd_finish(const int32_t *eta, int C, int K, int G, const floa
                              float kappa, const int32_t *kcur, double *usage, int32_t *k_next,
                              hipStream_t st);
 
+// ---- serving model: routing LP, prefix caching, configuration search -------------
+struct SvcArgs {
+    int C, G;
+    const int32_t *tau, *pp;
+    const float *Mcap, *Cc, *Bc;
+    const float *lam;
+    const int32_t *Lin, *Lpre;
+    const float *D;
+    double alpha, beta, t_ar, NL, c_gpu, c_slo, c_rej, kappa, u_max;
+    int J;
+};
+
+hipError_t launch_service_times(const SvcArgs &s, const int64_t *count, const int64_t *sum,
+                                const int64_t *sumsq, double *T, double *ET2, hipStream_t st);
+hipError_t launch_state(const SvcArgs &s, const double *T, const double *ET2, const double *pi,
+                        const int32_t *z, const int32_t *eta_c, const uint8_t *delta, double *Wq,
+                        double *cap, double *conc, double *mem, hipStream_t st);
+hipError_t launch_gather(const double *W, const int32_t *eta, const int32_t *k, int C, int K,
+                         double *Wc, int32_t *eta_c, hipStream_t st);
+hipError_t launch_cache(const double *conc, int n, uint8_t *delta, hipStream_t st);
+hipError_t launch_zero_u8(uint8_t *p, int n, hipStream_t st);
+// doubles of the LP1 work area (tableau and pivot column)
+size_t lp1_tableau_doubles(int C, int G);
+hipError_t launch_lp1(const SvcArgs &s, const double *Wc, const double *T, const double *Wq,
+                      const int32_t *z, const int32_t *eta_c, const uint8_t *delta, double *work,
+                      int32_t *basis, int max_pivots, double *pi_out, double *obj_out,
+                      int32_t *info, hipStream_t st);
+hipError_t launch_sweep(const double *W, const int32_t *eta, int C, int K, int G,
+                        const double *conc, const double *cap, double kappa, const int32_t *k_in,
+                        int32_t *k_out, uint8_t *feasible, hipStream_t st);
+hipError_t launch_converge(int C, int G, double tol, const int32_t *k_new, int32_t *k,
+                           const double *pi_new, double *pi, int32_t *flag, hipStream_t st);
+// doubles of the z-independent sums of the configuration search
+size_t config_pre_doubles(int C, int G);
+hipError_t launch_config_search(const SvcArgs &s, long long nz, const int32_t *gpus,
+                                const long long *ways, const double *Wc, const double *T,
+                                const double *ET2, const double *pi, const int32_t *eta_c,
+                                const uint8_t *delta_eval, double *pre_d, int32_t *pre_route,
+                                double *part_obj, long long *part_rank, long long *part_feas,
+                                int32_t *z, const uint8_t *delta_new, uint8_t *delta,
+                                double *best_obj, long long *best_rank, long long *n_feasible,
+                                int32_t *flag, hipStream_t st);
+hipError_t launch_state_objective(const SvcArgs &s, const double *T, const double *ET2,
+                                  const double *pi, const int32_t *z, const int32_t *eta_c,
+                                  const uint8_t *delta, const double *Wc, double *pre_d,
+                                  int32_t *pre_route, double *out, hipStream_t st);
+
 // ---- validation ----------------------------------------------------------------
 hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, int32_t *mn,
                              int32_t *mx, hipStream_t st);

@@ -400,3 +400,94 @@ def policy_workloads(trace: str = "burst", n_train: int = 1_000_000, n_eval: int
                   meta=dict(desc=f"{n_eval} fresh draws x shifts {list(shifts)}",
                             shifts=list(shifts), rhos=list(rhos)))
     return train, ev
+
+
+# ------------------------------------------------------- serving model ----
+
+@dataclass
+class Service:
+    """Serving-model inputs of Alg. 1 beyond the reservation data (Sec. 3.1-3.4).
+
+    The paper prints the cost ratios and kappa but not the service-time or
+    capacity constants; these are synthetic.
+    """
+    tau: np.ndarray      # int32 [G] tensor-parallel degree of configuration g
+    pp: np.ndarray       # int32 [G] pipeline-parallel degree
+    Mcap: np.ndarray     # float32 [G] KV capacity of one serving group, tokens
+    Cc: np.ndarray       # float32 [G] prefill rate, tokens/s
+    Bc: np.ndarray       # float32 [G] decode rate, tokens/s
+    lam: np.ndarray      # float32 [C] arrival rate, requests/s
+    Lin: np.ndarray      # int32 [C] input length, tokens
+    Lpre: np.ndarray     # int32 [C] shared (cacheable) prefix, tokens
+    D: np.ndarray        # float32 [C] latency SLO, s
+    alpha: float         # prefill work per input token (float32 value)
+    beta: float          # decode work per output token (float32 value)
+    t_ar: float          # all-reduce latency, s (float32 value)
+    NL: int              # layers
+    c_gpu: float         # cost per GPU-second (float32 values below)
+    c_slo: float         # cost per second of SLO excess
+    c_rej: float         # cost per rejected request
+    kappa: float         # memory-headroom factor
+    u_max: float         # largest admissible memory utilisation of a group
+    J: int               # GPU budget
+    z0: np.ndarray       # int32 [G] initial configuration counts
+
+    @property
+    def G(self) -> int:
+        return int(self.tau.shape[0])
+
+
+def serving_workload(C: int = 15, N: int = 100_000, J: int = 48, L: int = 8192, K: int = 2048,
+                     M: int = 256, seed: int = 6, configs=None):
+    """Reservation data of C classes plus a synthetic serving model.
+
+    Classes: lognormal output lengths (means log-spaced 20..600 tokens, sigma
+    U[0.6, 1.3]), clip [1, L]; c_w = 1, c_p = 10 (rho = 10); eps = 0.15 x
+    mean; arrival rates U[0.2, 2] requests/s; input 50..2000 tokens with a
+    10-60 % shared prefix; SLO U[2, 20] s.  Configurations: every (TP, PP) in
+    configs (default TP 1, 2, 4, 8 x PP 1, 2, 4) with KV capacity
+    ~4000 tokens per GPU, prefill ~8000 tokens/s and decode ~40 tokens/s per
+    request per unit of TP.  Cost weights in units of c_w: c_slo = 5,
+    c_rej = 5000, c_gpu = 0.5; kappa = 0.2 (the paper's printed ratios).
+    The start z0 adds one group of each configuration in turn while the
+    budget allows.
+    Returns (Workload, Service).
+    """
+    rng = np.random.default_rng(seed)
+    means = [20.0 * (30.0 ** (c / max(C - 1, 1))) for c in range(C)]
+    parts = [_clip_round(_lognormal_by_mean(rng, m, float(rng.uniform(0.6, 1.3)), N), 1, L)
+             for m in means]
+    offsets, xi = _csr(parts)
+    eps = _f32([0.15 * _mean(p) for p in parts])
+    w = Workload(f"serving-{C}x{N}", C, offsets, None, xi, np.full(C, L, np.int32),
+                 eta_grid(K, L), lam_grid(M), _f32([10.0] * C), _f32([1.0] * C), 1, eps,
+                 meta=dict(desc=f"{C} classes x {N} lognormal lengths (means 20..600), "
+                                f"rho = 10, eps = 0.15 x mean"))
+    if configs is None:
+        configs = [(t, p) for t in (1, 2, 4, 8) for p in (1, 2, 4)]
+    G = len(configs)
+    tau = np.array([t for t, _ in configs], np.int32)
+    pp = np.array([p for _, p in configs], np.int32)
+    gpus = (tau * pp).astype(np.float64)
+    Mcap = _f32(4000.0 * gpus * rng.uniform(0.8, 1.2, G))
+    Cc = _f32(8000.0 * tau * rng.uniform(0.8, 1.0, G))
+    Bc = _f32(40.0 * tau * rng.uniform(0.8, 1.0, G) / np.sqrt(pp))
+    lam = _f32(rng.uniform(0.2, 2.0, C))
+    Lin = rng.integers(50, 2000, C).astype(np.int32)
+    Lpre = (Lin * rng.uniform(0.1, 0.6, C)).astype(np.int32)
+    D = _f32(rng.uniform(2.0, 20.0, C))
+    z0 = np.zeros(G, np.int32)          # round-robin: one group of each configuration
+    used, grew = 0, True                 # in turn while the budget allows
+    while grew:
+        grew = False
+        for g in range(G):
+            if used + int(gpus[g]) <= J:
+                z0[g] += 1
+                used += int(gpus[g])
+                grew = True
+    svc = Service(tau, pp, Mcap, Cc, Bc, lam, Lin, Lpre, D,
+                  alpha=float(np.float32(1.0)), beta=float(np.float32(1.0)),
+                  t_ar=float(np.float32(2e-5)), NL=80, c_gpu=float(np.float32(0.5)),
+                  c_slo=float(np.float32(5.0)), c_rej=float(np.float32(5000.0)),
+                  kappa=float(np.float32(0.2)), u_max=float(np.float32(0.95)), J=J, z0=z0)
+    return w, svc
