@@ -177,6 +177,55 @@ def bench_policy(ctx, dev):
     }
 
 
+def bench_serving(ctx, dev):
+    """The rest of Alg. 1 (routing LP, prefix caching, configuration search)
+    on 15 classes x 1e5 samples, 12 (TP, PP) configurations, 48 GPUs."""
+    import numpy as np
+    import torch
+    import paper_2607_16892_amd as dro
+    from paper_2607_16892_amd import serving as gs
+    from workloads.configs import serving_workload
+    w, svc = serving_workload()
+    prob = dro.Problem.from_workload(w, dev)
+    s = gs.Service.from_model(svc, dev)
+    eps = torch.from_numpy(w.eps[: w.C].copy()).to(dev)
+    gs.dro_bcd_solve(ctx, prob, eps, s, svc.z0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    r = gs.dro_bcd_solve(ctx, prob, eps, s, svc.z0)
+    torch.cuda.synchronize()
+    solve_ms = (time.perf_counter() - t0) * 1e3
+    # the configuration search alone at the final state
+    tt = gs.bcd_service_times(ctx, prob, s)
+    k = r["k"].long()
+    ex = dro.dro_exact_table(ctx, prob, eps)
+    Wc = ex["W"][0].gather(1, k[:, None])[:, 0].contiguous()
+    eta_c = prob.eta[k].contiguous()
+    times = []
+    for _ in range(6):
+        z = r["z"].clone()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        cs = gs.bcd_config_search(ctx, w.C, s, Wc, tt["T"], tt["ET2"], r["pi"], eta_c, r["delta"], z)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    search_ms = float(np.median(times[1:]))
+    # |Z| = number of z >= 0 with sum_g z_g tau_g pp_g <= J (counted on the host)
+    gpus = [int(t) * int(p) for t, p in zip(svc.tau, svc.pp)]
+    ways = [1] * (svc.J + 1)
+    for gp in reversed(gpus):
+        ways = [sum(ways[b - u * gp] for u in range(b // gp + 1)) for b in range(svc.J + 1)]
+    nz = ways[svc.J]
+    return dict(workload=f"{w.name}: {w.meta['desc']}; {svc.G} (TP, PP) configurations, "
+                         f"J = {svc.J} GPUs",
+                solve_ms=solve_ms, info=r["info"], z=r["z"].cpu().tolist(),
+                objective=float(r["objective"].cpu()[0]),
+                config_search_ms=search_ms, configurations=nz,
+                configurations_per_s=nz / (search_ms / 1e3),
+                n_feasible=int(cs["n_feasible"].cpu()[0]))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,6 +237,8 @@ def main():
     ap.add_argument("--bcd-iters", type=int, default=3)
     ap.add_argument("--no-policy", action="store_true",
                     help="skip the reservation-policy comparison")
+    ap.add_argument("--no-serving", action="store_true",
+                    help="skip the routing / caching / configuration loop")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (scale reference for HBM byte counters)")
     args = ap.parse_args()
@@ -296,6 +347,10 @@ def main():
     if args.bcd_iters > 0:
         _log(f"block step, {args.bcd_iters} iterations")
         bcd = bench_bcd(ctx, dev, args.bcd_iters)
+    srv = None
+    if not args.no_serving:
+        _log("serving loop (routing LP, prefix caching, configuration search)")
+        srv = bench_serving(ctx, dev)
     pol = None
     if not args.no_policy:
         _log("policy comparison")
@@ -337,6 +392,7 @@ def main():
         "cpu_baseline": cpu,
         "block_step": bcd,
         "policy_comparison": pol,
+        "serving_loop": srv,
         "continuous_dual": cont,
         "exact_table": {"ms": exact_ms, "same_optimum_as_dense_path": same_k and same_w,
                         "note": "dro_exact_table: the same W table from value counts and prefix "

@@ -1,7 +1,7 @@
 """Write the stored oracle results of the benchmark workloads.
 
     python tests/golden/make_golden.py lognormal-1x1k lognormal-4x100k mixture-16x1M \
-        ratios-8x250k [drift-8x4M:ITERS] [policy-burst]
+        ratios-8x250k [drift-8x4M:ITERS] [policy-burst] [serving-15x100k]
 
 Calls only `oracle/` (exact 128-bit evaluation, value-grouped) and the seeded
 generator in `workloads/`.  Each file records the generator checksum of its
@@ -83,9 +83,25 @@ def golden_policy() -> dict:
                 cost_train=[[float(v).hex() for v in r] for r in t["cost_train"]])
 
 
+def golden_serving() -> dict:
+    from oracle import serving
+    from workloads.configs import serving_workload
+    params = dict(C=15, N=100_000, J=48, seed=6)
+    w, svc = serving_workload(**params)
+    t0 = time.time()
+    r = serving.solve(w, svc)
+    return dict(workload=w.name, params=params, checksum=w.checksum(),
+                oracle_seconds=round(time.time() - t0, 1), z=r["z"].tolist(), k=r["k"].tolist(),
+                delta=r["delta"].tolist(), pi=[[float(v).hex() for v in row] for row in r["pi"]],
+                objective=float(r["objective"]).hex(), outer=r["outer"], inner=r["inner"])
+
+
 def main(argv):
     for arg in argv:
-        if arg == "policy-burst":
+        if arg == "serving-15x100k":
+            data = golden_serving()
+            path = os.path.join(HERE, "serving-15x100k.json")
+        elif arg == "policy-burst":
             data = golden_policy()
             path = os.path.join(HERE, "policy-burst.json")
         elif arg.startswith("drift-8x4M"):

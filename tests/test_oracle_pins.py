@@ -6,6 +6,7 @@ invariance of the definition, or a textbook routine.  The pins are chosen so
 that a dropped term, a wrong sign or index, or a transposed operand in
 dro_oracle.c fails at least one of them.
 """
+import itertools
 import math
 from fractions import Fraction as F
 
@@ -547,3 +548,143 @@ def test_P19_table_structure():
         xs = ev.samples_of(s * tr.C).astype(np.int64)
         assert t["cost"][i_max, s, 0] == float(F(600 * xs.size - int(xs.sum()), xs.size))
         assert np.all(t["cover"][i_max, s] == xs.size)
+
+
+# --------------------------------------------------------------- P20-P24 ---
+# The serving-model oracle (oracle/serving.py) of the rest of Alg. 1.
+
+def _serving_tiny(seed, C=3, J=8, configs=((1, 1), (2, 1), (2, 2))):
+    from workloads.configs import serving_workload
+    return serving_workload(C=C, N=400, J=J, L=600, K=61, M=12, seed=seed, configs=list(configs))
+
+
+def test_P20_waiting_time_reduces_to_mm1():
+    # Pollaczek-Khinchin with exponential service (second moment 2 T^2, Cs2 = 1)
+    # is the M/M/1 wait u T / (1 - u).
+    from oracle import serving as osv
+    w, svc = _serving_tiny(1)
+    T, _ = osv.service_times(svc, w)
+    ET2 = 2.0 * T * T
+    pi = np.zeros((w.C, svc.G))
+    pi[0, :] = 0.3                     # one class per group: a single exponential
+    z = np.ones(svc.G, np.int64)
+    mem = np.array([0.3, 0.6, 0.9]) * svc.Mcap.astype(np.float64)
+    Wq = osv.queue(svc, T, ET2, pi, z, mem)
+    for g in range(svc.G):
+        lam = svc.lam.astype(np.float64)
+        tb = float((lam * pi[:, g] * T[:, g]).sum() / (lam * pi[:, g]).sum())
+        u = mem[g] / float(svc.Mcap[g])
+        assert Wq[g] == pytest.approx(u * tb / (1.0 - u), rel=1e-12)
+
+
+def test_P21_prefix_caching_saves_memory_exactly_when_concurrency_exceeds_the_margin():
+    # Caching class c's prefix on g changes mem_g by Lpre (1 - (1 + kappa) conc_cg):
+    # it saves memory iff (1 + kappa) conc_cg > 1 (Block 2 caches at conc > 1).
+    from oracle import serving as osv
+    w, svc = _serving_tiny(2)
+    T, _ = osv.service_times(svc, w)
+    rng = np.random.default_rng(2)
+    pi = rng.uniform(0.0, 0.5, (w.C, svc.G))
+    z = np.array([1, 2, 1], np.int64)
+    eta_c = rng.integers(0, 300, w.C)
+    d0 = np.zeros((w.C, svc.G), np.uint8)
+    conc = osv.concurrency(svc, T, pi, z)
+    for c in range(w.C):
+        for g in range(svc.G):
+            d1 = d0.copy()
+            d1[c, g] = 1
+            diff = osv.memory(svc, T, pi, z, eta_c, d1)[g] - osv.memory(svc, T, pi, z, eta_c, d0)[g]
+            want = float(svc.Lpre[c]) * (1.0 - (1.0 + float(svc.kappa)) * conc[c, g])
+            assert diff == pytest.approx(want, rel=1e-9, abs=1e-9)
+
+
+def test_P22_routing_lp_beats_every_sampled_feasible_routing():
+    from oracle import serving as osv
+    w, svc = _serving_tiny(3)
+    T, ET2 = osv.service_times(svc, w)
+    z = np.array([2, 1, 1], np.int64)
+    eta_c = np.array([50, 120, 300])
+    delta = np.zeros((w.C, svc.G), np.uint8)
+    Wq = np.array([0.2, 0.5, 1.0])
+    Wc = np.array([300.0, 900.0, 2500.0])
+    pi, obj = osv.routing_lp(svc, Wc, T, Wq, z, eta_c, delta)
+
+    def lp_obj(p):
+        tot = 0.0
+        for c in range(w.C):
+            lin = sum(p[c, g] * (Wc[c] + float(svc.c_gpu) * float(svc.tau[g] * svc.pp[g]) * T[c, g]
+                                 - float(svc.c_rej)) for g in range(svc.G))
+            h = sum(p[c, g] * (Wq[g] + T[c, g] - float(svc.D[c])) for g in range(svc.G))
+            tot += float(svc.lam[c]) * (lin + float(svc.c_slo) * max(h, 0.0) + float(svc.c_rej))
+        return tot
+
+    assert lp_obj(pi) == pytest.approx(obj, rel=1e-9)
+    assert np.all(pi.sum(axis=1) <= 1 + 1e-9)
+    assert np.all(osv.memory(svc, T, pi, z, eta_c, delta) <= float(svc.u_max) * svc.Mcap * (1 + 1e-9))
+    rng = np.random.default_rng(3)
+    lim = float(svc.u_max) * svc.Mcap.astype(np.float64)
+    for _ in range(400):
+        p = rng.dirichlet(np.ones(svc.G + 1), w.C)[:, :svc.G]
+        mem = osv.memory(svc, T, p, z, eta_c, delta)
+        if np.all(mem <= lim):
+            assert obj <= lp_obj(p) + 1e-9 * abs(obj)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_P23_configuration_search_equals_brute_force(seed):
+    # the vectorised scan (numpy over z) against the plain loop over
+    # itertools.product: the same minimiser, objective bits, rank and count
+    from oracle import serving as osv
+    w, svc = _serving_tiny(10 + seed, C=4, J=12)
+    T, ET2 = osv.service_times(svc, w)
+    rng = np.random.default_rng(seed)
+    pi = rng.dirichlet(np.ones(svc.G + 1), w.C)[:, :svc.G] * 0.4
+    delta = (rng.random((w.C, svc.G)) < 0.3).astype(np.uint8)
+    eta_c = rng.integers(0, 200, w.C)
+    Wc = rng.uniform(50, 2000, w.C)
+    a = osv.config_search(svc, Wc, T, ET2, pi, eta_c, delta)
+    b = osv.config_search_vec(svc, Wc, T, ET2, pi, eta_c, delta)
+    assert np.array_equal(a[0], b[0]) and a[1] == b[1] and a[2] == b[2] and a[3] == b[3]
+    # the count of Z is the number of z with sum z_g tau_g pp_g <= J
+    n = sum(1 for _ in itertools.product(*[range(svc.J // int(svc.tau[g] * svc.pp[g]) + 1)
+                                         for g in range(svc.G)])
+            if sum(zz * int(svc.tau[g] * svc.pp[g]) for g, zz in enumerate(_)) <= svc.J)
+    assert osv.config_space_array(svc).shape[0] == n
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_P24_sweep_agrees_with_the_block_step(seed):
+    # the fp64 sweep of LP2 and the oracle's block step (pinned by P13) on the
+    # same float32-representable capacities and concurrencies
+    from oracle import serving as osv
+    from workloads.configs import Groups
+    w = _tiny(900 + seed, C=4, N=(60, 31, 90, 77), L=600, K=33, M=9, E=1, with_groups=True, G=3)
+    S = oracle.S_exact(w)
+    W = oracle.W_table(w, S)[0][0]
+    k_prev = oracle.bcd_init(w)
+    o = oracle.bcd_step(w, W, k_prev)
+    conc = w.groups.conc.astype(np.float64).reshape(w.C, -1)
+    k, ok = osv.sweep(W, w.eta, conc, w.groups.cap.astype(np.float64), w.groups.kappa, k_prev)
+    assert np.array_equal(k, o["k_next"]) and np.array_equal(ok, o["feasible"].astype(bool))
+
+
+@pytest.mark.parametrize("seed", [6, 7])
+def test_P24_alg1_ends_blockwise_optimal(seed):
+    # Prop. 4.3: at termination no block improves on its own: Block 3 keeps z,
+    # Block 2 reproduces delta, and the reservations are a fixed point of LP2.
+    from oracle import serving as osv
+    from workloads.configs import serving_workload
+    w, svc = serving_workload(C=4, N=2000, J=12, K=129, M=16, seed=seed,
+                              configs=[(1, 1), (2, 1), (4, 1), (2, 2)])
+    r = osv.solve(w, svc, max_outer=20)
+    if r["outer"] >= 20:
+        pytest.skip("the loop did not terminate on this instance")
+    T, ET2 = r["T"], r["ET2"]
+    Wc = np.array([r["W1"][c, r["k"][c]] for c in range(w.C)])
+    eta_c = w.eta[r["k"]]
+    assert np.array_equal(osv.prefix_cache(svc, T, r["pi"], r["z"]), r["delta"])
+    zb, best, _, _ = osv.config_search_vec(svc, Wc, T, ET2, r["pi"], eta_c, r["delta"])
+    assert osv.state_objective(svc, Wc, T, ET2, r["pi"], r["z"], eta_c, r["delta"]) == best
+    conc, cap = osv.lp2_inputs(svc, T, r["pi"], r["z"], r["delta"])
+    k2, _ = osv.sweep(r["W1"], w.eta, conc, cap, svc.kappa, r["k"])
+    assert np.array_equal(k2, r["k"])

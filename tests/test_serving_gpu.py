@@ -220,3 +220,28 @@ def test_alg1_matches_oracle(ctx, dev, seed):
     assert abs(obj - ref["objective"]) <= 1e-9 * abs(ref["objective"])
     assert r["info"]["outer"] == ref["outer"] and r["info"]["inner"] == ref["inner"]
     assert r["info"]["status"] & (1 | 2 | 4) == 0
+
+
+def test_alg1_full_size_against_stored_oracle(ctx, dev):
+    # 15 classes x 1e5 samples, K = 2048, M = 256, 12 configurations, 48 GPUs
+    # (747,788 configurations per search)
+    import json
+    import os
+    import torch
+    from paper_2607_16892_amd import serving as gs
+    path = os.path.join(os.path.dirname(__file__), "golden", "serving-15x100k.json")
+    gold = json.load(open(path))
+    w, svc = serving_workload(**gold["params"])
+    assert w.checksum() == gold["checksum"]
+    prob, s = _setup(ctx, dev, w, svc)
+    r = gs.dro_bcd_solve(ctx, prob, _t(w.eps[: w.C], np.float32, dev), s, svc.z0)
+    torch.cuda.synchronize()
+    print("  info", r["info"], flush=True)
+    assert r["z"].cpu().numpy().tolist() == gold["z"]
+    assert r["k"].cpu().numpy().tolist() == gold["k"]
+    assert r["delta"].cpu().numpy().tolist() == gold["delta"]
+    ref_pi = np.array([[float.fromhex(v) for v in row] for row in gold["pi"]])
+    assert np.max(np.abs(r["pi"].cpu().numpy() - ref_pi)) <= 1e-7
+    obj, ref = float(r["objective"].cpu()[0]), float.fromhex(gold["objective"])
+    assert abs(obj - ref) <= 1e-9 * abs(ref)
+    assert (r["info"]["outer"], r["info"]["inner"]) == (gold["outer"], gold["inner"])
