@@ -393,7 +393,7 @@ int dro_create(int hip_device, dro_ctx **out)
     if (hipGetDeviceProperties(&prop, hip_device) == hipSuccess && prop.multiProcessorCount > 0)
         ctx->num_cu = prop.multiProcessorCount;
     ctx->dense_bpc = dense_blocks_per_cu();
-    if (hist_prepare() != hipSuccess) {
+    if (hist_prepare() != hipSuccess || lp1_prepare() != hipSuccess) {
         (void)hipGetLastError();
         delete ctx;
         return DRO_EHIP;

@@ -183,6 +183,8 @@ hipError_t launch_cache(const double *conc, int n, uint8_t *delta, hipStream_t s
 hipError_t launch_zero_u8(uint8_t *p, int n, hipStream_t st);
 // doubles of the LP1 work area (tableau and pivot column)
 size_t lp1_tableau_doubles(int C, int G);
+// allow lp1_kernel its dynamic LDS (once per device)
+hipError_t lp1_prepare();
 hipError_t launch_lp1(const SvcArgs &s, const double *Wc, const double *T, const double *Wq,
                       const int32_t *z, const int32_t *eta_c, const uint8_t *delta, double *work,
                       int32_t *basis, int max_pivots, double *pi_out, double *obj_out,

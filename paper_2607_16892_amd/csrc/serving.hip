@@ -161,9 +161,10 @@ __global__ void zero_u8_kernel(uint8_t *p, int n)
 // ((m + 1) x (n + m + 1) doubles), the basis in `basis` (m ints).
 __global__ __launch_bounds__(kSvcThreads) void lp1_kernel(
     SvcArgs s, const double *Wc, const double *T, const double *Wq, const int32_t *z,
-    const int32_t *eta_c, const uint8_t *delta, double *tab, int32_t *basis, double *col,
-    int max_pivots, double *pi_out, double *obj_out, int32_t *info)
+    const int32_t *eta_c, const uint8_t *delta, double *tab_g, int32_t *basis, double *col_g,
+    int in_lds, int max_pivots, double *pi_out, double *obj_out, int32_t *info)
 {
+    extern __shared__ double lds_tab[];  // (m + 1) * w + (m + 1) doubles when in_lds
     __shared__ double red_d[kSvcThreads];
     __shared__ int red_i[kSvcThreads];
     __shared__ double sh_scale;
@@ -171,6 +172,8 @@ __global__ __launch_bounds__(kSvcThreads) void lp1_kernel(
     const int C = s.C, G = s.G;
     const int nv = C * G + C, m = 2 * C + G, w = nv + m + 1;
     const double kap = 1.0 + s.kappa;
+    double *tab = in_lds ? lds_tab : tab_g;
+    double *col = in_lds ? lds_tab + (long long)(m + 1) * w : col_g;
 
     // build: constraint rows, slack identity, right-hand sides
     for (long long e = t; e < (long long)(m + 1) * w; e += nt) tab[e] = 0.0;
@@ -283,11 +286,11 @@ __global__ __launch_bounds__(kSvcThreads) void lp1_kernel(
         double *prow = tab + (long long)rsel * w;
         for (int j = t; j < w; j += nt) prow[j] = prow[j] / piv;
         __syncthreads();
-        for (long long e = t; e < (long long)(m + 1) * w; e += nt) {
-            const int r = (int)(e / w), j = (int)(e % w);
-            if (r == rsel) continue;
+        for (int r = 0; r <= m; ++r) {
             const double f = col[r];
-            if (f != 0.0) tab[e] = tab[e] - f * prow[j];
+            if (r == rsel || f == 0.0) continue;
+            double *row = tab + (long long)r * w;
+            for (int j = t; j < w; j += nt) row[j] = row[j] - f * prow[j];
         }
         __syncthreads();
         if (t == 0) basis[rsel] = jin;
@@ -673,6 +676,14 @@ hipError_t launch_zero_u8(uint8_t *p, int n, hipStream_t st)
     return hipGetLastError();
 }
 
+constexpr size_t kLp1LdsBytes = 152 * 1024;  // dynamic LDS for the tableau (of 160 KB)
+
+hipError_t lp1_prepare()
+{
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(lp1_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLp1LdsBytes);
+}
+
 size_t lp1_tableau_doubles(int C, int G)
 {
     const long long nv = (long long)C * G + C, m = 2LL * C + G;
@@ -686,8 +697,12 @@ hipError_t launch_lp1(const SvcArgs &s, const double *Wc, const double *T, const
 {
     const long long nv = (long long)s.C * s.G + s.C, m = 2LL * s.C + s.G;
     double *tab = work, *col = work + (m + 1) * (nv + m + 1);
-    hipLaunchKernelGGL(lp1_kernel, dim3(1), dim3(kSvcThreads), 0, st, s, Wc, T, Wq, z, eta_c,
-                       delta, tab, basis, col, max_pivots, pi_out, obj_out, info);
+    // the tableau lives in LDS when it fits (one workgroup, every pivot touches all of it)
+    const size_t bytes = lp1_tableau_doubles(s.C, s.G) * sizeof(double);
+    const int in_lds = bytes <= kLp1LdsBytes ? 1 : 0;
+    hipLaunchKernelGGL(lp1_kernel, dim3(1), dim3(kSvcThreads), in_lds ? bytes : 0, st, s, Wc, T,
+                       Wq, z, eta_c, delta, tab, basis, col, in_lds, max_pivots, pi_out, obj_out,
+                       info);
     return hipGetLastError();
 }
 
