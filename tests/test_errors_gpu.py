@@ -150,3 +150,53 @@ def test_entry_points_reject_null_outputs(ctx, dev):
     assert lib.dro_exact_table(ctx.handle, ct.byref(ps), 1, None, None, None, None, None, None,
                                None, stream) == EINVAL
     assert lib.bcd_block_step(ctx.handle, ct.byref(ps), None, None, None, None, stream) == EINVAL
+
+
+def test_serving_entry_points_reject_bad_arguments(ctx, dev):
+    import torch
+    from paper_2607_16892_amd import serving as gs
+    from workloads.configs import serving_workload
+    w, svc = serving_workload(C=3, N=500, J=8, K=33, M=8, configs=[(1, 1), (2, 1)], seed=1)
+    lib = ctx._lib
+    stream = ct.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    s = gs.Service.from_model(svc, dev)
+    C, G = w.C, svc.G
+    T = torch.zeros((C, G), dtype=torch.float64, device=dev)
+    pi = torch.zeros((C, G), dtype=torch.float64, device=dev)
+    z = torch.ones(G, dtype=torch.int32, device=dev)
+    eta_c = torch.zeros(C, dtype=torch.int32, device=dev)
+    delta = torch.zeros((C, G), dtype=torch.uint8, device=dev)
+    Wq = torch.zeros(G, dtype=torch.float64, device=dev)
+    out = torch.zeros(4 * C * G + 8, dtype=torch.float64, device=dev)
+
+    def lp(ss):
+        return lib.bcd_routing_lp(ctx.handle, C, ct.byref(ss), out.data_ptr(), T.data_ptr(),
+                                  Wq.data_ptr(), z.data_ptr(), eta_c.data_ptr(),
+                                  delta.data_ptr(), pi.data_ptr(), out.data_ptr(),
+                                  z.data_ptr(), stream)
+
+    ss = s.struct()
+    ss.u_max = 1.0
+    assert lp(ss) == EINVAL                  # the wait would not stay finite
+    ss = s.struct()
+    ss.G = 33
+    assert lp(ss) == ELIMIT
+    ss = s.struct()
+    ss.J = 5000
+    assert lp(ss) == ELIMIT
+    ss = s.struct()
+    ss.Lin = None
+    assert lp(ss) == EINVAL
+    ss = s.struct()
+    bad = np.array([0, 1], np.int32)
+    ss.tau_h = bad.ctypes.data
+    assert lp(ss) == EINVAL                  # a configuration with no GPU
+    assert lib.bcd_reservation_sweep(ctx.handle, C, 4, None, None, G, None, None, 0.2, None, None,
+                                      None, stream) == EINVAL
+    assert lib.bcd_prefix_cache(ctx.handle, 0, G, None, None, stream) == EINVAL
+    zz = z.clone()
+    ss = s.struct()
+    assert lib.bcd_config_search(ctx.handle, C, ct.byref(ss), None, None, None, None, None, None,
+                                 zz.data_ptr(), None, None, None, stream) == EINVAL
+    torch.cuda.synchronize()
+    assert torch.equal(zz, z)
