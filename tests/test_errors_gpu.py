@@ -128,6 +128,12 @@ def test_host_checks_and_untouched_outputs(ctx, dev):
     bad = prob.struct()
     bad.K = 40000
     assert call(bad) == ELIMIT
+    # a class beyond 2^26 samples (rejected from the host offsets alone)
+    big = w.offsets.copy()
+    big[1:] += (1 << 26) + 1 - int(w.offsets[1])
+    bad = prob.struct()
+    bad.offsets_h = big.ctypes.data
+    assert call(bad) == ELIMIT
     torch.cuda.synchronize()
     assert torch.all(W == 7.0), "a rejected call wrote its output"
     assert "NULL" in ctx.last_error() or "K=" in ctx.last_error() or ctx.last_error()

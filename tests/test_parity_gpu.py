@@ -227,3 +227,32 @@ def test_exact_table_large_config_against_stored_oracle(ctx, dev, name):
     for c, row in gold["W_rows"].items():
         ref = np.array([float.fromhex(v) for v in row])
         assert np.array_equal(g["W"][0, int(c)].view(np.uint64), ref.view(np.uint64)), f"class {c}"
+
+
+# ---------------------------------------------------------- maximum sizes ----
+# The largest grids and segments the library accepts (K = 2^15 + 1 grid points,
+# M = 65536 multipliers, 2^26 samples in one class), each against the oracle.
+
+def test_max_reservation_grid(ctx, dev):
+    w = random_workload(seed=41, C=1, N=(3000,), L=32768, K=32769, M=16, E=2)
+    assert np.array_equal(w.eta, np.arange(32769))
+    check_against_oracle(w, run_gpu(ctx, w, dev))
+
+
+def test_max_multiplier_grid(ctx, dev):
+    w = random_workload(seed=42, C=2, N=(500, 300), L=1000, K=8, M=65536, E=1)
+    assert np.all(np.diff(w.lam.astype(np.float64)) > 0)
+    check_against_oracle(w, run_gpu(ctx, w, dev))
+
+
+def test_max_class_size(ctx, dev):
+    from workloads.configs import Workload
+    from workloads import eta_grid, lam_grid
+    n = 1 << 26
+    rng = np.random.default_rng(43)
+    xi = rng.integers(0, 32769, n, dtype=np.int32)
+    L = 32768
+    w = Workload("max-class", 1, np.array([0, n], np.int64), None, xi, np.array([L], np.int32),
+                 eta_grid(5, L), lam_grid(4), np.array([8.0], np.float32),
+                 np.array([1.0], np.float32), 1, np.array([100.0], np.float32))
+    check_against_oracle(w, run_gpu(ctx, w, dev))
