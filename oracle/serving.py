@@ -9,12 +9,12 @@ the paper leaves open marked "reading":
   T[c,g]   = pp_g alpha Lin_c / Cc_g + beta E[xi_c] / Bc_g + NL tau_g t_ar      service time
   ET2[c,g] = A^2 + 2 A B E[xi_c] + B^2 E[xi_c^2] with A = pp_g alpha Lin_c / Cc_g
              + NL tau_g t_ar and B = beta / Bc_g: second moment of the service
-             time over the samples (reading: the paper's "empirical service-time
-             distribution")
+             time over the samples (reading: the paper takes the variability of
+             the service time from the training samples)
   conc[c,g] = lam_c T_cg pi_cg / z_g                 concurrent requests (Little's law)
   mem[g]   = (1 + kappa) (sum_c lam_c T_cg pi_cg (Lin_c + eta_c - delta_cg Lpre_c)) / z_g
              + sum_c delta_cg Lpre_c                 KV tokens in use (Sec. 3.4)
-  util[g]  = mem_g / Mcap_g  (reading: the memory utilisation under which the
+  util[g]  = mem_g / Mcap_g  (reading: the memory utilisation, at which the
              paper's simulator evaluates the queue; with the compute utilisation
              sum_c conc_cg, which the queue needs below 1, no concurrency could
              exceed 1 and Block 2 would never cache)
