@@ -66,13 +66,20 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
     __shared__ long long red[kThreads];
 
     const DensePlan pl = a.plan;
-    long long b = blockIdx.x;
-    const int p = (int)(b % pl.P);
-    b /= pl.P;
+    // Workgroups are dispatched to the XCDs in turn (block i to XCD i mod 8), so
+    // XCD x is given one contiguous run of logical blocks; logical blocks that
+    // read the same sample slice (one class and slice, every grid and multiplier
+    // tile) are consecutive, so each slice is fetched into one XCD's L2.
+    const long long nb = gridDim.x;
+    const int xcd = (int)(blockIdx.x % kXcds);
+    const long long q = nb / kXcds, r = nb % kXcds;
+    long long b = xcd * q + min((long long)xcd, r) + blockIdx.x / kXcds;
     const int tm = (int)(b % pl.tiles_m);
     b /= pl.tiles_m;
     const int tk = (int)(b % pl.tiles_k);
     b /= pl.tiles_k;
+    const int p = (int)(b % pl.P);
+    b /= pl.P;
     const int c = (int)b;
 
     const int t = threadIdx.x;

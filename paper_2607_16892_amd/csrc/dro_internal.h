@@ -18,6 +18,7 @@ constexpr int kTK = 1;
 constexpr int kTM = 32;
 constexpr int kTileN = 1024;  // samples staged per LDS tile
 constexpr int kRun = 64;      // fp32 run length before the fp64 fold
+constexpr int kXcds = 8;      // accelerator complex dies of one MI355X (one L2 each)
 
 struct DensePlan {
     int lanes_m, lanes_k;  // lane grid inside a block
