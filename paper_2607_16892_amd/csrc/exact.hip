@@ -18,6 +18,12 @@ namespace dro {
 
 __device__ __forceinline__ int seg_of_x(const int32_t *seg, int c) { return seg ? seg[c] : c; }
 
+#define HIPRET(expr)                                 \
+    do {                                             \
+        const hipError_t e_ = (expr);                \
+        if (e_ != hipSuccess) return e_;             \
+    } while (0)
+
 // v * 2^33 for a binary32 v in [2^-10, 2^7] (exact integer below 2^41).
 __device__ __forceinline__ int64_t fix33(float v)
 {
@@ -656,58 +662,112 @@ namespace dro {
 // evaluated in 128-bit integers in units of 2^-33: exact.
 
 // Per segment: cnt[v] = #{x <= v} (u32) and sum[v] = sum of the samples <= v
-// (u64), from the value histogram; one 1024-thread block per segment.
-__global__ __launch_bounds__(1024) void prefix_kernel(const uint32_t *hist, uint32_t *cnt,
-                                                      uint64_t *sum)
+// (u64), from the value histogram.  Block (segment, chunk) handles 4096 bins:
+// it sums the bins before its chunk (coalesced), stages the chunk in LDS
+// (padded to spread the per-thread runs over the banks), scans it (16
+// consecutive bins per thread, then across threads) and stores each thread's
+// run of prefixes.
+constexpr int kPrefixChunk = 4096;
+constexpr int kPrefixThreads = 256;
+constexpr int kPrefixPer = kPrefixChunk / kPrefixThreads;  // 16
+
+__device__ __forceinline__ int pad32(int j) { return j + (j >> 5); }
+
+__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *hist, uint32_t *cnt,
+                                                                uint64_t *sum)
 {
-    const int s = blockIdx.x, t = threadIdx.x;
-    constexpr int per = (kHistBins + 1023) / 1024;
+    __shared__ uint32_t hc[kPrefixChunk + kPrefixChunk / 32];
+    __shared__ uint64_t rc[kPrefixThreads], rs[kPrefixThreads];
+    constexpr int kChunks = (kHistBins + kPrefixChunk - 1) / kPrefixChunk;
+    const int ch = (int)(blockIdx.x % kChunks), s = (int)(blockIdx.x / kChunks), t = threadIdx.x;
     const uint32_t *h = hist + (long long)s * kHistBins;
-    uint32_t *oc = cnt + (long long)s * kHistBins;
-    uint64_t *os = sum + (long long)s * kHistBins;
-    const int b0 = t * per, b1 = min(kHistBins, b0 + per);
-    uint64_t pc = 0, ps = 0;
-    for (int v = b0; v < b1; ++v) {
-        pc += h[v];
-        ps += (uint64_t)h[v] * (uint64_t)v;
+    const int v0 = ch * kPrefixChunk, v1 = min(kHistBins, v0 + kPrefixChunk), n = v1 - v0;
+    uint64_t bc = 0, bs = 0;  // everything before the chunk
+    for (int v = t; v < v0; v += kPrefixThreads) {
+        const uint64_t x = h[v];
+        bc += x;
+        bs += x * (uint64_t)v;
     }
-    __shared__ uint64_t sc[1024], ss[1024];
-    sc[t] = pc;
-    ss[t] = ps;
+    for (int j = t; j < n; j += kPrefixThreads) hc[pad32(j)] = h[v0 + j];
+    rc[t] = bc;
+    rs[t] = bs;
     __syncthreads();
-    for (int w = 1; w < 1024; w <<= 1) {  // inclusive scans
-        const uint64_t ac = t >= w ? sc[t - w] : 0, as = t >= w ? ss[t - w] : 0;
-        __syncthreads();
-        sc[t] += ac;
-        ss[t] += as;
+    for (int w = kPrefixThreads / 2; w > 0; w >>= 1) {
+        if (t < w) {
+            rc[t] += rc[t + w];
+            rs[t] += rs[t + w];
+        }
         __syncthreads();
     }
-    uint64_t c = sc[t] - pc, x = ss[t] - ps;
-    for (int v = b0; v < b1; ++v) {
-        c += h[v];
-        x += (uint64_t)h[v] * (uint64_t)v;
-        oc[v] = (uint32_t)c;
-        os[v] = x;
+    const uint64_t base_c = rc[0], base_s = rs[0];
+    __syncthreads();
+    const int a = t * kPrefixPer;
+    uint64_t lc = 0, ls = 0;
+    for (int i = 0; i < kPrefixPer; ++i) {
+        const int j = a + i;
+        if (j < n) {
+            const uint64_t x = hc[pad32(j)];
+            lc += x;
+            ls += x * (uint64_t)(v0 + j);
+        }
+    }
+    rc[t] = lc;
+    rs[t] = ls;
+    __syncthreads();
+    for (int w = 1; w < kPrefixThreads; w <<= 1) {  // inclusive scans
+        const uint64_t ac = t >= w ? rc[t - w] : 0, as = t >= w ? rs[t - w] : 0;
+        __syncthreads();
+        rc[t] += ac;
+        rs[t] += as;
+        __syncthreads();
+    }
+    uint64_t c = base_c + rc[t] - lc, x = base_s + rs[t] - ls;
+    uint32_t *gc = cnt + (long long)s * kHistBins + v0;
+    uint64_t *gs = sum + (long long)s * kHistBins + v0;
+    for (int i = 0; i < kPrefixPer; ++i) {
+        const int j = a + i;
+        if (j < n) {
+            const uint64_t hv = hc[pad32(j)];
+            c += hv;
+            x += hv * (uint64_t)(v0 + j);
+            gc[j] = (uint32_t)c;
+            gs[j] = x;
+        }
     }
 }
 
-__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)  // b > 0
+hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st)
 {
-    int64_t q = a / b;
-    if ((a % b != 0) && (a < 0)) --q;
+    const long long blocks = (long long)S * ((kHistBins + kPrefixChunk - 1) / kPrefixChunk);
+    hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st, hist,
+                       cnt, sum);
+    return hipGetLastError();
+}
+
+// floor(a / b) for b > 0 and |a| < 2^62: a double estimate (within 1 of the
+// quotient for the ranges used here) corrected with exact integer products.
+__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)
+{
+    int64_t q = (int64_t)floor((double)a / (double)b);
+    while (q * b > a) --q;
+    while ((q + 1) * b <= a) ++q;
     return q;
 }
 
-// Thread per (c, k): exact S for every m, exact J for every radius row, and
-// the minimum over m with the lowest m (W, m_star).
-__global__ __launch_bounds__(256) void exact_table_kernel(
+// Block per (c, k), thread per multiplier (m = t, t + 256, ...): exact S,
+// exact J for every radius row, and the minimum over m with the lowest m
+// (W, m_star), radius rows in groups of 8 reduced across the block.
+constexpr int kTableThreads = 256;
+
+__global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
     const float *lam, const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt,
     const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star)
 {
-    const long long ck = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (ck >= (long long)C * K) return;
-    const int c = (int)(ck / K), k = (int)(ck % K);
+    __shared__ double rv[8][kTableThreads];
+    __shared__ int rm[8][kTableThreads];
+    const long long ck = blockIdx.x;
+    const int c = (int)(ck / K), k = (int)(ck % K), t = threadIdx.x;
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
     const int64_t L = L_[c], eta = eta_[k];
@@ -725,39 +785,62 @@ __global__ __launch_bounds__(256) void exact_table_kernel(
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             best[q] = __builtin_inf();
-            bm[q] = 0;
+            bm[q] = 0x7fffffff;
             ev[q] = (e0 + q < E) ? (double)eps[(long long)(e0 + q) * C + c] : 0.0;
         }
-        for (int m = 0; m < M; ++m) {
+        for (int m = t; m < M; m += kTableThreads) {
             const int64_t G = fix33(lam[m]);
             const int64_t A1 = G < CW ? G : CW, A2 = G < CP ? G : CP;
             const int64_t num = B - Cc + A2 * L;
-            int64_t t = floor_div(num, A1 + A2);
-            t = t < -1 ? -1 : (t > tmax ? tmax : t);
-            const __int128 ct = t >= 0 ? (__int128)cn[t] : 0;
-            const __int128 st = t >= 0 ? (__int128)sm[t] : 0;
+            int64_t tt = floor_div(num, A1 + A2);
+            tt = tt < -1 ? -1 : (tt > tmax ? tmax : tt);
+            const __int128 ct = tt >= 0 ? (__int128)cn[tt] : 0;
+            const __int128 st = tt >= 0 ? (__int128)sm[tt] : 0;
             const __int128 S = (__int128)B * ct - (__int128)A1 * st +
                                (__int128)(Cc - A2 * L) * ((__int128)N - ct) +
                                (__int128)A2 * (sum_all - st);
             const unsigned __int128 u = (unsigned __int128)S;
             const double q_ = __ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), Nd);
             const double lm = (double)lam[m];
+            const int nq = E - e0;
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
+                if (q >= nq) break;
                 const double J = __dadd_rn(__dmul_rn(lm, ev[q]), q_);
-                if (J < best[q]) {
+                if (J < best[q]) {  // m ascending: the first minimiser of this thread
                     best[q] = J;
                     bm[q] = m;
                 }
             }
         }
+        const int nq = E - e0 < 8 ? E - e0 : 8;
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            if (e0 + q >= E) break;
-            const long long o = ((long long)(e0 + q) * C + c) * K + k;
-            W[o] = best[q];
-            m_star[o] = bm[q];
+            rv[q][t] = best[q];
+            rm[q][t] = bm[q];
         }
+        __syncthreads();
+        for (int w = kTableThreads / 2; w > 0; w >>= 1) {
+            if (t < w) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    if (q >= nq) break;
+                    const double v2 = rv[q][t + w];
+                    const int m2 = rm[q][t + w];
+                    if (v2 < rv[q][t] || (v2 == rv[q][t] && m2 < rm[q][t])) {
+                        rv[q][t] = v2;
+                        rm[q][t] = m2;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        if (t < 8 && e0 + t < E) {
+            const long long o = ((long long)(e0 + t) * C + c) * K + k;
+            W[o] = rv[t][0];
+            m_star[o] = rm[t][0];
+        }
+        __syncthreads();
     }
 }
 
@@ -811,10 +894,10 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
                               int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
 {
-    hipLaunchKernelGGL(prefix_kernel, dim3(S), dim3(1024), 0, st, hist, cnt, sum);
+    HIPRET(launch_prefix(hist, S, cnt, sum, st));
     const long long n = (long long)C * K;
-    hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                       offsets, seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,
+    hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)n), dim3(kTableThreads), 0, st, offsets,
+                       seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,
                        (const uint64_t *)sum, E, C, K, M, W, m_star);
     if (k_star)
         hipLaunchKernelGGL(table_argmin_kernel, dim3(E * C), dim3(256), 0, st, (const double *)W,
@@ -931,7 +1014,7 @@ hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, co
                                   int K, uint32_t *cnt, uint64_t *sum, double *W, double *gamma,
                                   hipStream_t st)
 {
-    hipLaunchKernelGGL(prefix_kernel, dim3(S), dim3(1024), 0, st, hist, cnt, sum);
+    HIPRET(launch_prefix(hist, S, cnt, sum, st));
     const long long n = (long long)E * C * K;
     hipLaunchKernelGGL(continuous_dual_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                        offsets, seg, L, eta, c_p, c_w, eps, (const uint32_t *)cnt,
@@ -1041,7 +1124,7 @@ hipError_t launch_reservation_cost(const int64_t *offsets, const int32_t *seg, c
                                    const int32_t *eta_r, uint32_t *cnt, uint64_t *sum,
                                    double *cost, int64_t *cover, hipStream_t st)
 {
-    hipLaunchKernelGGL(prefix_kernel, dim3(S), dim3(1024), 0, st, hist, cnt, sum);
+    HIPRET(launch_prefix(hist, S, cnt, sum, st));
     const long long n = (long long)R * C;
     hipLaunchKernelGGL(reservation_cost_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
                        st, offsets, seg, c_p, c_w, (const uint32_t *)cnt, (const uint64_t *)sum,
