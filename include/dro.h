@@ -16,6 +16,10 @@
  * Prop. 4.2 on the grid), the critical-fractile quantile (Prop. 4.2,
  * eps = 0) and one capacity-constrained reservation update of
  * Block 1 of Alg. 1 under the memory-capacity constraint (Sec. 3.4).
+ * Further entry points: the same table exactly from value counts, the
+ * dual over continuous gamma, per-class moments and the cost of given
+ * reservations (the policy comparison of Sec. 5), and the rest of Alg. 1
+ * (routing LP, prefix caching, configuration search; last section).
  *
  * Conventions, binding on every entry point:
  *  - Array arguments are DEVICE memory owned by the caller unless the field
@@ -23,7 +27,9 @@
  *    caller pointer after the call returns; scratch memory belongs to the ctx.
  *  - Every compute call is asynchronous on `stream` (a hipStream_t; NULL is
  *    the null stream): it returns after enqueueing, outputs are valid after
- *    the stream is synchronised.  dro_validate is synchronous.
+ *    the stream is synchronised.  dro_validate, dro_take_flags and
+ *    dro_bcd_solve (whose loop reads its decisions on the host) are
+ *    synchronous.
  *  - Return value 0 = DRO_OK, negative = error.  Nothing is thrown across the
  *    ABI.  On an error found on the host no kernel is launched and no output
  *    is written; dro_last_error(ctx) holds the detail.
