@@ -226,6 +226,33 @@ def bench_serving(ctx, dev):
                 n_feasible=int(cs["n_feasible"].cpu()[0]))
 
 
+def bench_alg1_scaling(ctx, dev):
+    """Solve time of the whole Alg. 1 loop over the problem sizes of Table 3
+    (classes x configurations x samples), synthetic serving model."""
+    import torch
+    import paper_2607_16892_amd as dro
+    from paper_2607_16892_amd import serving as gs
+    from workloads.configs import serving_workload
+    sizes = [(3, 4, 100, 8), (4, 4, 150, 8), (5, 5, 200, 8), (6, 6, 300, 8), (8, 6, 500, 8),
+             (10, 8, 1000, 48), (15, 12, 2000, 48)]
+    every = [(t, p) for t in (1, 2, 4, 8) for p in (1, 2, 4)]
+    rows = []
+    for C, G, N, J in sizes:
+        w, svc = serving_workload(C=C, N=N, J=J, K=2048, M=256, seed=20 + C, configs=every[:G])
+        prob = dro.Problem.from_workload(w, dev)
+        s = gs.Service.from_model(svc, dev)
+        eps = torch.from_numpy(w.eps[: w.C].copy()).to(dev)
+        gs.dro_bcd_solve(ctx, prob, eps, s, svc.z0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = gs.dro_bcd_solve(ctx, prob, eps, s, svc.z0)
+        torch.cuda.synchronize()
+        rows.append({"classes": C, "configurations": G, "samples": N, "gpus": J,
+                     "solve_ms": (time.perf_counter() - t0) * 1e3, "outer": r["info"]["outer"],
+                     "inner": r["info"]["inner"], "status": r["info"]["status"]})
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -351,6 +378,7 @@ def main():
     if not args.no_serving:
         _log("serving loop (routing LP, prefix caching, configuration search)")
         srv = bench_serving(ctx, dev)
+        srv["scaling"] = bench_alg1_scaling(ctx, dev)
     pol = None
     if not args.no_policy:
         _log("policy comparison")
