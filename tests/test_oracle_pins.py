@@ -688,3 +688,59 @@ def test_P24_alg1_ends_blockwise_optimal(seed):
     conc, cap = osv.lp2_inputs(svc, T, r["pi"], r["z"], r["delta"])
     k2, _ = osv.sweep(r["W1"], w.eta, conc, cap, svc.kappa, r["k"])
     assert np.array_equal(k2, r["k"])
+
+
+def test_P24_sweep_takes_the_lowest_minimiser_on_ties():
+    # a flat table: every grid point is a minimiser, the lowest one is taken
+    # (the tie rule of the reservation argmin), and a binding bound caps it
+    from oracle import serving as osv
+    W = np.zeros((2, 9))
+    eta = np.arange(0, 90, 10)
+    conc = np.array([[1.0], [0.0]])
+    k, ok = osv.sweep(W, eta, conc, np.array([1000.0]), 0.0, np.array([8, 8]))
+    assert k.tolist() == [0, 0] and ok.all()
+    W[0, :] = [5, 5, 3, 3, 3, 4, 1, 1, 2]
+    k, ok = osv.sweep(W, eta, conc, np.array([1000.0]), 0.0, np.array([0, 0]))
+    assert k[0] == 6                                   # lowest of the tied minima
+    k, ok = osv.sweep(W, eta, conc, np.array([45.0]), 0.0, np.array([0, 0]))
+    assert k[0] == 2                                   # eta <= 45: grid points 0..4
+
+
+def test_P21_block2_caches_exactly_where_caching_saves_memory_at_zero_margin():
+    # with kappa = 0, caching the prefix of (c, g) lowers the memory of g iff
+    # conc_cg > 1, which is Block 2's rule
+    from dataclasses import replace
+    from oracle import serving as osv
+    w, svc = _serving_tiny(5)
+    svc = replace(svc, kappa=0.0)
+    T, _ = osv.service_times(svc, w)
+    z = np.array([1, 1, 2], np.int64)
+    # routings that give the concurrencies 0.3 .. 2.5 (some just below and above 1)
+    target = np.array([0.3, 0.6, 0.9, 0.99, 1.01, 1.2, 1.6, 2.0, 2.5]).reshape(w.C, svc.G)
+    pi = target * z[None, :] / (svc.lam.astype(np.float64)[:, None] * T)
+    eta_c = np.zeros(w.C, np.int64)
+    d0 = np.zeros((w.C, svc.G), np.uint8)
+    delta = osv.prefix_cache(svc, T, pi, z)
+    for c in range(w.C):
+        for g in range(svc.G):
+            d1 = d0.copy()
+            d1[c, g] = 1
+            saves = osv.memory(svc, T, pi, z, eta_c, d1)[g] < osv.memory(svc, T, pi, z, eta_c, d0)[g]
+            assert bool(delta[c, g]) == saves, (c, g)
+    assert 0 < delta.sum() < delta.size
+
+
+def test_P18_mean_plus_spread_on_a_hand_worked_sample():
+    # samples 1, 2, 3, 10: mean 4, population variance 12.5, sigma 3.5355...:
+    # LP+1sigma = ceil(7.5355) = 8, LP+2sigma = ceil(11.071) = 12, Mean = 4
+    from oracle import policies
+    from workloads.configs import Workload
+    xs = np.array([1, 2, 3, 10], np.int32)
+    w = Workload("hand", 1, np.array([0, 4], np.int64), None, xs, np.array([20], np.int32),
+                 np.arange(21, dtype=np.int32), np.array([1.0], np.float32),
+                 np.array([10.0], np.float32), np.array([1.0], np.float32), 1,
+                 np.array([0.0], np.float32))
+    eta = policies.reservations(w, (0.0,))
+    row = dict(zip(policies.policy_names((0.0,)), eta[:, 0]))
+    assert row["Mean"] == 4 and row["LP+1sigma"] == 8 and row["LP+2sigma"] == 12
+    assert row["P90"] == 10 and row["Max"] == 20     # ceil(0.9 * 4) = 4th smallest
