@@ -299,8 +299,10 @@ int bcd_queue_state(dro_ctx *ctx, int32_t C, const dro_service *svc, const doubl
  * with the reservations, z and delta fixed and the wait Wq (device [G]) frozen
  * at the incoming state, subject to sum_g pi_cg <= 1, the SLO slack rows and
  * mem_g <= u_max Mcap_g.  Wc [C] holds each class's worst-case cost at its
- * reservation.  Dense simplex with Bland's rule in one workgroup (fp64, rows
- * scaled by their largest coefficient).  lp_objective (device double [1]) is
+ * reservation.  Dense simplex in one workgroup (fp64, rows scaled by their
+ * largest coefficient): the most negative reduced cost enters, and after 20
+ * degenerate pivots in a row Bland's rule takes over until the objective
+ * moves, so the method cannot cycle.  lp_objective (device double [1]) is
  * the objective at the solution with s_c at its optimum; info (device int32
  * [2]) = {pivots, status}: 0 optimal, 1 pivot limit, 2 infeasible at pi = 0
  * (prefixes alone exceed a capacity), 3 unbounded. */

@@ -30,6 +30,7 @@ namespace {
 constexpr int kSvcThreads = 256;
 constexpr double kMemSlack = 1.0 + 1e-9;  // relative slack of a configuration's memory check
 constexpr double kEtaSlack = 1e-6;        // tokens of slack of the sweep's reservation bound
+constexpr int kLpDegenerateRun = 20;      // degenerate pivots before the simplex turns to Bland's rule
 
 __device__ __forceinline__ double block_min_d(double v, double *red)
 {
@@ -56,6 +57,40 @@ __device__ __forceinline__ int block_min_i(int v, int *red)
         __syncthreads();
     }
     const int r = red[0];
+    __syncthreads();
+    return r;
+}
+
+// Lexicographic minimum of (key, idx) over the block (smallest key, then the
+// smallest idx), carrying aux along: shuffles inside each wave, then one pass
+// over the per-wave results in LDS.
+struct KeyIdx {
+    double key;
+    int idx, aux;
+};
+
+__device__ __forceinline__ KeyIdx block_min_key(double k, int i, int a, double *sk, int *si,
+                                                int *sa)
+{
+    for (int off = 32; off > 0; off >>= 1) {
+        const double k2 = __shfl_xor(k, off);
+        const int i2 = __shfl_xor(i, off), a2 = __shfl_xor(a, off);
+        if (k2 < k || (k2 == k && i2 < i)) {
+            k = k2;
+            i = i2;
+            a = a2;
+        }
+    }
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+    if (lane == 0) {
+        sk[wid] = k;
+        si[wid] = i;
+        sa[wid] = a;
+    }
+    __syncthreads();
+    KeyIdx r{sk[0], si[0], sa[0]};
+    for (int q = 1; q < nw; ++q)
+        if (sk[q] < r.key || (sk[q] == r.key && si[q] < r.idx)) r = KeyIdx{sk[q], si[q], sa[q]};
     __syncthreads();
     return r;
 }
@@ -152,8 +187,10 @@ __global__ void zero_u8_kernel(uint8_t *p, int n)
 
 // ------------------------------------------------------------------- LP1 ----
 // min c^T x over x >= 0 with A x <= b, b >= 0, by the simplex method on a
-// dense tableau with Bland's rule (smallest entering index, ties of the ratio
-// test to the smallest basic index), which cannot cycle.  Variables: pi[c,g]
+// dense tableau.  The entering column has the most negative reduced cost;
+// after 20 degenerate pivots in a row the rule becomes Bland's (smallest
+// entering index) until a pivot moves the objective, so the method cannot
+// cycle.  Ties of the ratio test go to the smallest basic index.  Variables: pi[c,g]
 // at c*G + g (fixed at 0 where z_g = 0), then s_c.  Rows: sum_g pi_cg <= 1;
 // sum_g pi_cg (Wq_g + T_cg - D_c) - s_c <= 0; memory of every g with z_g > 0
 // (empty rows otherwise).  Each row is scaled by its largest coefficient, the
@@ -167,6 +204,8 @@ __global__ __launch_bounds__(kSvcThreads) void lp1_kernel(
     extern __shared__ double lds_tab[];  // (m + 1) * w + (m + 1) doubles when in_lds
     __shared__ double red_d[kSvcThreads];
     __shared__ int red_i[kSvcThreads];
+    __shared__ double wk_d[kSvcThreads / 64];
+    __shared__ int wk_i[kSvcThreads / 64], wk_a[kSvcThreads / 64];
     __shared__ double sh_scale;
     const int t = threadIdx.x, nt = blockDim.x;
     const int C = s.C, G = s.G;
@@ -239,19 +278,24 @@ __global__ __launch_bounds__(kSvcThreads) void lp1_kernel(
     __syncthreads();
 
     int status = anybad ? 2 : 0;  // 0 optimal, 1 pivot limit, 2 infeasible start, 3 unbounded
-    int pivots = 0;
+    int pivots = 0, degenerate = 0;
     const double tol_d = 1e-12, tol_p = 1e-11;
     while (status == 0) {
-        // entering column: smallest index with a negative reduced cost
+        // entering column: the most negative reduced cost (lowest index on ties);
+        // after a run of degenerate pivots, the lowest index with a negative
+        // reduced cost (Bland's rule, which cannot cycle) until the objective moves
+        const bool bland = degenerate >= kLpDegenerateRun;
+        double dmin = 0.0;
         int cand = 0x7fffffff;
         for (int j = t; j < nv + m; j += nt) {
             if (j < C * G && z[j % G] <= 0) continue;
-            if (tab[(long long)m * w + j] < -tol_d) {
+            const double d = tab[(long long)m * w + j];
+            if (d < -tol_d && (bland ? cand == 0x7fffffff : d < dmin)) {
+                dmin = d;
                 cand = j;
-                break;
             }
         }
-        const int jin = block_min_i(cand, red_i);
+        const int jin = block_min_key(bland ? 0.0 : dmin, cand, 0, wk_d, wk_i, wk_a).idx;
         if (jin == 0x7fffffff) break;  // optimal
         if (pivots >= max_pivots) {
             status = 1;
@@ -271,26 +315,37 @@ __global__ __launch_bounds__(kSvcThreads) void lp1_kernel(
                 }
             }
         }
-        const double qmin = block_min_d(best, red_d);
-        const int bmin = block_min_i(best == qmin ? bb : 0x7fffffff, red_i);
-        if (bmin == 0x7fffffff) {
+        const KeyIdx lv = block_min_key(best, bb, brow, wk_d, wk_i, wk_a);
+        if (lv.idx == 0x7fffffff) {
             status = 3;
             break;
         }
-        // the row holding basic variable bmin with the minimum ratio
-        const int rsel = block_min_i((best == qmin && bb == bmin) ? brow : 0x7fffffff, red_i);
-        // pivot on (rsel, jin)
+        const int rsel = lv.aux;  // the row of the leaving basic variable
+        degenerate = lv.key == 0.0 ? degenerate + 1 : 0;
+        // pivot on (rsel, jin): each thread updates its own columns of every
+        // row, reading eight rows before writing them back
         for (int r = t; r <= m; r += nt) col[r] = tab[(long long)r * w + jin];
         __syncthreads();
         const double piv = col[rsel];
         double *prow = tab + (long long)rsel * w;
-        for (int j = t; j < w; j += nt) prow[j] = prow[j] / piv;
-        __syncthreads();
-        for (int r = 0; r <= m; ++r) {
-            const double f = col[r];
-            if (r == rsel || f == 0.0) continue;
-            double *row = tab + (long long)r * w;
-            for (int j = t; j < w; j += nt) row[j] = row[j] - f * prow[j];
+        for (int j = t; j < w; j += nt) {
+            const double pj = prow[j] / piv;
+            prow[j] = pj;
+            for (int r0 = 0; r0 <= m; r0 += 8) {
+                double v[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int r = r0 + q;
+                    v[q] = r <= m ? tab[(long long)r * w + j] : 0.0;
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int r = r0 + q;
+                    if (r > m || r == rsel) continue;
+                    const double f = col[r];
+                    if (f != 0.0) tab[(long long)r * w + j] = v[q] - f * pj;
+                }
+            }
         }
         __syncthreads();
         if (t == 0) basis[rsel] = jin;
@@ -338,8 +393,8 @@ __global__ __launch_bounds__(kSvcThreads) void sweep_kernel(
     const double *W, const int32_t *eta, int C, int K, int G, const double *conc,
     const double *cap, double kappa, const int32_t *k_in, int32_t *k_out, uint8_t *feasible)
 {
-    __shared__ double red_d[kSvcThreads];
-    __shared__ int red_i[kSvcThreads];
+    __shared__ double wk_d[kSvcThreads / 64];
+    __shared__ int wk_i[kSvcThreads / 64], wk_a[kSvcThreads / 64];
     const int t = threadIdx.x, nt = blockDim.x;
     const double onek = 1.0 + kappa;
     for (int c = t; c < C; c += nt) k_out[c] = min(max(k_in[c], 0), K - 1);
@@ -355,12 +410,12 @@ __global__ __launch_bounds__(kSvcThreads) void sweep_kernel(
             const double b = (cap[g] - onek * other) / (onek * cc);
             if (b < bound) bound = b;
         }
-        bound = block_min_d(bound, red_d);
+        bound = block_min_key(bound, 0, 0, wk_d, wk_i, wk_a).key;
         // largest k with eta[k] <= bound (eta ascending)
         int cand = -1;
         for (int kk = t; kk < K; kk += nt)
             if ((double)eta[kk] <= bound + kEtaSlack) cand = kk;
-        const int kmax = -block_min_i(-cand, red_i);
+        const int kmax = -block_min_key(0.0, -cand, 0, wk_d, wk_i, wk_a).idx;
         const int hi = kmax < 0 ? 0 : kmax;
         // lowest argmin of W[c, 0..hi]
         const double *wr = W + (long long)c * K;
@@ -371,8 +426,7 @@ __global__ __launch_bounds__(kSvcThreads) void sweep_kernel(
                 bv = wr[kk];
                 bk = kk;
             }
-        const double vmin = block_min_d(bv, red_d);
-        const int kbest = block_min_i(bv == vmin ? bk : 0x7fffffff, red_i);
+        const int kbest = block_min_key(bv, bk, 0, wk_d, wk_i, wk_a).idx;
         if (t == 0) {
             k_out[c] = kbest;
             if (feasible) feasible[c] = kmax >= 0 ? 1 : 0;
