@@ -253,6 +253,14 @@ def bench_alg1_scaling(ctx, dev):
     return rows
 
 
+def _platform(dev) -> dict:
+    import torch
+    p = torch.cuda.get_device_properties(dev)
+    return {"device": p.name, "arch": getattr(p, "gcnArchName", None),
+            "compute_units": p.multi_processor_count, "hip": torch.version.hip,
+            "torch": torch.__version__}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -322,7 +330,8 @@ def main():
     t1 = time.perf_counter()
     flags = ctx.take_flags()
     ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
-    dense_ms = float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+    launch_times = [a.elapsed_time(b) for a, b in pairs]
+    dense_ms = float(np.mean(launch_times))
     evals = w.evals
     value = evals / (ms_step / 1e3)
     achieved = evals * FLOPS_PER_EVAL / (dense_ms / 1e3) / 1e12
@@ -408,7 +417,8 @@ def main():
                      "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / FP32_PEAK_TFLOPS,
                      "traffic": cnt["hbm_bytes_per_launch"] if cnt else None,
-                     "launch_ms": dense_ms, "flops_per_eval": FLOPS_PER_EVAL,
+                     "launch_ms": dense_ms, "launch_ms_median": float(np.median(launch_times)),
+                     "launch_ms_min": float(np.min(launch_times)), "flops_per_eval": FLOPS_PER_EVAL,
                      "evals_per_launch": evals,
                      "note": "frac counts the paper-form 7 fp32 ops per evaluation; the kernel's "
                              "exact two-line form issues valu_instr_per_eval instructions, so "
@@ -428,6 +438,7 @@ def main():
                                 "so it is reported beside the metric, not as it",
                         "equivalent_evals_per_s": evals / (exact_ms / 1e3)},
         "flags": flags,
+        "platform": _platform(dev),
     }
     print(json.dumps(line), flush=True)
     ctx.close()

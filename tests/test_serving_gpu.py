@@ -130,6 +130,47 @@ def test_routing_lp_matches_highs(ctx, dev, seed):
         assert np.all(memg <= float(svc.u_max) * svc.Mcap.astype(np.float64) * (1 + 1e-12))
 
 
+@pytest.mark.parametrize("seed", [7, 8])
+def test_routing_lp_degenerate(ctx, dev, seed):
+    """Identical classes and a wait that makes every SLO row tight at pi = 0:
+    many optimal routings and many degenerate pivots.  The optimal objective
+    is unique (1e-9 relative to HiGHS) and the GPU routing is feasible and
+    attains it."""
+    import torch
+    from paper_2607_16892_amd import serving as gs
+    w, svc = serving_workload(C=12, N=3000, J=24, K=257, M=32, configs=SMALL, seed=seed)
+    for name in ("lam", "Lin", "Lpre", "D"):
+        getattr(svc, name)[:] = getattr(svc, name)[0]
+    s = gs.Service.from_model(svc, dev)
+    T, ET2 = osv.service_times(svc, w)
+    T = np.repeat(T[:1], w.C, axis=0)
+    z = np.ones(svc.G, np.int32)
+    delta = np.zeros((w.C, svc.G), np.uint8)
+    eta_c = np.full(w.C, 200, np.int32)
+    Wq = float(svc.D[0]) - T[0]            # Wq_g + T_cg - D_c = 0 for every row
+    Wc = np.full(w.C, 800.0)
+    ref_pi, ref_obj = osv.routing_lp(svc, Wc, T, Wq, z, eta_c, delta)
+    r = gs.bcd_routing_lp(ctx, w.C, s, _t(Wc, np.float64, dev), _t(T, np.float64, dev),
+                          _t(Wq, np.float64, dev), _t(z, np.int32, dev),
+                          _t(eta_c, np.int32, dev), _t(delta, np.uint8, dev))
+    torch.cuda.synchronize()
+    info = r["info"].cpu().numpy()
+    assert info[1] == 0, f"simplex status {info[1]}"
+    obj = float(r["objective"].cpu().numpy()[0])
+    assert abs(obj - ref_obj) <= 1e-9 * abs(ref_obj), (obj, ref_obj)
+    pi = r["pi"].cpu().numpy()
+    assert np.all(pi >= 0.0) and np.all(pi.sum(axis=1) <= 1.0 + 1e-12)
+    memg = osv.memory(svc, T, pi, z, eta_c, delta)
+    assert np.all(memg <= float(svc.u_max) * svc.Mcap.astype(np.float64) * (1 + 1e-12))
+    slack = np.maximum((pi * (Wq[None, :] + T - svc.D[:, None].astype(np.float64))).sum(1), 0.0)
+    lam = svc.lam.astype(np.float64)
+    gpu = (svc.tau.astype(np.float64) * svc.pp)[None, :] * T
+    val = float(np.sum(lam[:, None] * pi * (Wc[:, None] + float(svc.c_gpu) * gpu
+                                            - float(svc.c_rej)))
+                + np.sum(lam * float(svc.c_slo) * slack) + np.sum(lam * float(svc.c_rej)))
+    assert abs(val - ref_obj) <= 1e-9 * abs(ref_obj), (val, ref_obj)
+
+
 def test_routing_lp_infeasible_start(ctx, dev):
     import torch
     from paper_2607_16892_amd import serving as gs
