@@ -417,6 +417,11 @@ def main():
                      "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / FP32_PEAK_TFLOPS,
                      "traffic": cnt["hbm_bytes_per_launch"] if cnt else None,
+                     "algorithmic_bytes": 4 * int(w.offsets[-1]) + 8 * w.C * w.K * w.M,
+                     "traffic_note": "algorithmic bytes = the int32 samples read once plus the fp64 "
+                                     "S table written once; the launch writes S as P sample-slice "
+                                     "partials (P = 3 on mixture-16x1M, so that the grid fills whole "
+                                     "waves) that a deterministic reduce sums",
                      "launch_ms": dense_ms, "launch_ms_median": float(np.median(launch_times)),
                      "launch_ms_min": float(np.min(launch_times)), "flops_per_eval": FLOPS_PER_EVAL,
                      "evals_per_launch": evals,
