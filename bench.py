@@ -40,10 +40,10 @@ VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 
 # comments and layout stripped, identified by the hash prefix) and are
 # reported as null for any other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "2ec7f114ec76f772",
+    "dense_code_sha256_16": "5c6380b918757116",
     "workload": "mixture-16x1M",
-    "valu_instr_per_eval": 2.1029,       # SQ_INSTS_VALU x 64 / evaluations
-    "hbm_bytes_per_launch": 264147.875 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
+    "valu_instr_per_eval": 2.0580,       # SQ_INSTS_VALU x 64 / evaluations
+    "hbm_bytes_per_launch": 263918.5 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
     "source": "profiles/dense_kernel_mixture-16x1M_counters.md",
 }
 

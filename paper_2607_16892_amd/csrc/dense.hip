@@ -133,12 +133,17 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
 
         for (int u0 = 0; u0 < len; u0 += kRun) {
             const int cnt = min(kRun, len - u0);
+            // the run's first sample initialises the accumulators
             float acc[kTK][kTM];
+            auto first = [&](float x) {
 #pragma unroll
-            for (int i = 0; i < kTK; ++i)
+                for (int i = 0; i < kTK; ++i) {
+                    const float u = fmaf(x, sc, eoff[i]);
 #pragma unroll
-                for (int j = 0; j < kTM; ++j) acc[i][j] = 0.0f;
-
+                    for (int j = 0; j < kTM; ++j)
+                        acc[i][j] = __builtin_amdgcn_fmed3f(u + add[i][j], 0.0f, 1.0f);
+                }
+            };
             auto step = [&](float x) {
 #pragma unroll
                 for (int i = 0; i < kTK; ++i) {
@@ -149,7 +154,10 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
                 }
             };
 
-            int u = 0;
+            first(xs[u0]);
+            int u = 1;
+            for (; u < 4 && u < cnt; ++u) step(xs[u0 + u]);
+#pragma unroll 4
             for (; u + 4 <= cnt; u += 4) {
                 const float4 x4 = *reinterpret_cast<const float4 *>(&xs[u0 + u]);
                 step(x4.x);
