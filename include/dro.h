@@ -139,8 +139,9 @@ int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out);
  *   W[e,c,k]  = min over m of  RN(RN(lam_m eps[e,c]) + RN(S[c,k,m] / N_c))
  *   m_star    = the lowest m attaining it.
  * S may be NULL (kept in the ctx workspace); m_star may be NULL.
- * W is accurate to about 1e-7 relative; use dro_argmin_reservation for the
- * exact optimum. */
+ * W is within 1e-5 relative of its exact value (typically about 1e-7; 2e-6
+ * when every sample sits at the kink of phi); use dro_argmin_reservation for
+ * the exact optimum. */
 int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps, double *W,
                   int32_t *m_star, double *S, dro_stream_t stream);
 
