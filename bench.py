@@ -36,20 +36,23 @@ VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 
 
 # Hardware-counter figures of the dense kernel on the 16 x 1e6 workload, from
 # profiles/dense_kernel_mixture-16x1M_counters.md.  They describe one version of the
-# dense kernel's code (csrc/dense.hip and the constants of csrc/dro_internal.h,
-# comments and layout stripped, identified by the hash prefix) and are
+# dense kernel's code and launch plan (csrc/dense.hip, the constants of
+# csrc/dro_internal.h and plan_dense of csrc/api.hip, comments and layout
+# stripped, identified by the hash prefix) and are
 # reported as null for any other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "5c6380b918757116",
+    "dense_code_sha256_16": "9a9f7ae608d0f09a",
     "workload": "mixture-16x1M",
-    "valu_instr_per_eval": 2.0580,       # SQ_INSTS_VALU x 64 / evaluations
-    "hbm_bytes_per_launch": 263918.5 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
+    "valu_instr_per_eval": 2.0597,       # SQ_INSTS_VALU x 64 / evaluations
+    "hbm_bytes_per_launch": 1638327.5 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
     "source": "profiles/dense_kernel_mixture-16x1M_counters.md",
 }
 
 
 def dense_code_hash() -> str:
-    """Hash of the dense kernel's code with comments and whitespace removed."""
+    """Hash of the dense kernel's code and of its launch plan (the plan_dense
+    function of csrc/api.hip, which sets the number of sample slices and so
+    the partial-sum traffic), comments and whitespace removed."""
     import hashlib
     import re
     def code(name):
@@ -58,7 +61,10 @@ def dense_code_hash() -> str:
         return re.sub(r"//[^\n]*", " ", text)
 
     consts = [ln for ln in code("dro_internal.h").splitlines() if "constexpr" in ln]
-    text = code("dense.hip") + "\n" + "\n".join(consts)
+    api = code("api.hip")
+    i = api.index("constexpr long long kMinWaves")
+    plan = api[i:api.index("return pl;", i)]
+    text = code("dense.hip") + "\n" + "\n".join(consts) + "\n" + plan
     return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
 
 
@@ -423,9 +429,11 @@ def main():
                      "traffic": cnt["hbm_bytes_per_launch"] if cnt else None,
                      "algorithmic_bytes": 4 * int(w.offsets[-1]) + 8 * w.C * w.K * w.M,
                      "traffic_note": "algorithmic bytes = the int32 samples read once plus the fp64 "
-                                     "S table written once; the launch writes S as P sample-slice "
-                                     "partials (P = 3 on mixture-16x1M, so that the grid fills whole "
-                                     "waves) that a deterministic reduce sums",
+                                     "S table written once; the samples are read once, and the launch "
+                                     "writes S as P sample-slice partials (P = 24 on mixture-16x1M, "
+                                     "so that the grid runs 32 short waves of blocks) that a "
+                                     "deterministic reduce sums: 1.6 GB at about 7 GB/s, which the "
+                                     "VALU-bound kernel does not feel",
                      "launch_ms": dense_ms, "launch_ms_median": float(np.median(launch_times)),
                      "launch_ms_min": float(np.min(launch_times)), "flops_per_eval": FLOPS_PER_EVAL,
                      "evals_per_launch": evals,
