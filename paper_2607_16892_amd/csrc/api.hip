@@ -80,8 +80,10 @@ size_t rup(size_t v) { return (v + 255) & ~size_t(255); }
 int ensure_ws(dro_ctx *ctx, size_t need, hipStream_t st)
 {
     if (need <= ctx->ws_size) return DRO_OK;
-    // earlier work on this stream may still read the old buffer
-    HIPCHK(hipStreamSynchronize(st));
+    // earlier work may still read the old buffer: on this stream, or on another
+    // stream the context was used on before (growth is rare, so wait for all)
+    (void)st;
+    HIPCHK(hipDeviceSynchronize());
     if (ctx->ws) {
         HIPCHK(hipFree(ctx->ws));
         ctx->ws = nullptr;
