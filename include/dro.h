@@ -70,8 +70,10 @@ enum {
     DRO_ELIMIT = -5  /* beyond the exactness limits above                                */
 };
 
-/* Status bits accumulated on the device by the argmin refine; read and
- * cleared with dro_take_flags. */
+/* Status bits accumulated on the device by the exact argmin; read and
+ * cleared with dro_take_flags.  They report how an optimum was found, not an
+ * error: where the screening band did not settle it, the exact table of that
+ * (e, c) did, and the result is the same exact optimum either way. */
 enum {
     DRO_FLAG_BAND_FULL = 1u,   /* a screening band held more candidates than the refine keeps */
     DRO_FLAG_BAND_MARGIN = 2u  /* the exact optimum sat too close to the band edge            */
@@ -151,8 +153,12 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
  *                    the exact sum of phi (128-bit fixed point), round-to-nearest-even
  *   m_at_star[e,c] = lowest m attaining it (may be NULL).
  * `S` is the table written by dro_cost_eval for the same problem; it is used to
- * screen candidates, which are then evaluated exactly.  Ties go to the lowest k,
- * then the lowest m. */
+ * screen candidates (every (k, m) within 1e-4 relative of the screened
+ * minimum, at most 256 per (e, c)), which are then evaluated exactly.  Where
+ * the band overflows or the exact optimum sits near its edge, the exact table
+ * of dro_exact_table settles that (e, c) instead and a DRO_FLAG_* bit is
+ * raised; the result is exact either way.  Ties go to the lowest k, then the
+ * lowest m. */
 int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
                            const double *S, const int32_t *k_max, int32_t *k_star, double *W_star,
                            int32_t *m_at_star, dro_stream_t stream);

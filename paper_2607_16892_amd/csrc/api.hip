@@ -242,28 +242,77 @@ size_t dense_bytes(const dro_problem *p, const DensePlan &pl, bool need_S)
     return b;
 }
 
+long long max_segment(const dro_problem *p)
+{
+    long long max_seg = 0;
+    for (int s = 0; s < p->S; ++s)
+        max_seg = std::max(max_seg, (long long)(p->offsets_h[s + 1] - p->offsets_h[s]));
+    return max_seg;
+}
+
+struct QuantBufs {
+    uint32_t *hist, *part;
+    int B;
+};
+
+size_t quantile_bytes(const dro_problem *p, int num_cu)
+{
+    const int B = hist_parts(p->S, max_segment(p), num_cu);
+    return rup((size_t)p->S * kHistBins * 4) + (B > 1 ? rup((size_t)p->S * B * kHistBins * 4) : 0);
+}
+
+QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
+{
+    QuantBufs q;
+    q.B = hist_parts(p->S, max_segment(p), num_cu);
+    q.hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
+    q.part = q.B > 1 ? ar.take<uint32_t>((size_t)p->S * q.B * kHistBins) : nullptr;
+    return q;
+}
+
+// Scratch of the exact argmin: the screening band, the exact partial sums of
+// its candidates, and the exact table that settles any (e, c) whose band did
+// not (histogram, prefix counts and sums, and the [E*C][K] table).
 struct RefineBufs {
     int32_t *cand, *count;
     double *thresh, *chunk_min;
     uint64_t *part;
+    int32_t *need;
+    uint32_t *any;
+    QuantBufs qb;
+    uint32_t *cnt;
+    uint64_t *sum;
+    double *Wt;
+    int32_t *mt;
 };
 
 size_t band_chunks(int K) { return (size_t)(K + kBandKC - 1) / kBandKC; }
 
-size_t refine_bytes(int EC, int P, int K)
+size_t refine_bytes(const dro_problem *p, int EC, int P, int num_cu)
 {
+    const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
     return rup((size_t)EC * kBandCap * 4) + rup((size_t)EC * 4) + rup((size_t)EC * 8) +
-           rup((size_t)EC * band_chunks(K) * 8) + rup((size_t)EC * kBandCap * P * 16);
+           rup((size_t)EC * band_chunks(p->K) * 8) + rup((size_t)EC * kBandCap * P * 16) +
+           rup((size_t)EC * 4) + rup(4) + quantile_bytes(p, num_cu) + rup(bins * 4) +
+           rup(bins * 8) + rup(eck * 8) + rup(eck * 4);
 }
 
-RefineBufs take_refine(Arena &ar, int EC, int P, int K)
+RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int P, int num_cu)
 {
     RefineBufs r;
+    const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
     r.cand = ar.take<int32_t>((size_t)EC * kBandCap);
     r.count = ar.take<int32_t>(EC);
     r.thresh = ar.take<double>(EC);
-    r.chunk_min = ar.take<double>((size_t)EC * band_chunks(K));
+    r.chunk_min = ar.take<double>((size_t)EC * band_chunks(p->K));
     r.part = ar.take<uint64_t>((size_t)EC * kBandCap * P * 2);
+    r.need = ar.take<int32_t>(EC);
+    r.any = ar.take<uint32_t>(1);
+    r.qb = take_quantile(ar, p, num_cu);
+    r.cnt = ar.take<uint32_t>(bins);
+    r.sum = ar.take<uint64_t>(bins);
+    r.Wt = ar.take<double>(eck);
+    r.mt = ar.take<int32_t>(eck);
     return r;
 }
 
@@ -273,6 +322,8 @@ int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, cons
                int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
 {
     const int EC = E * p->C;
+    HIPCHK(launch_fill_u32(reinterpret_cast<uint32_t *>(rb.need), EC, 0u, st));
+    HIPCHK(launch_fill_u32(rb.any, 1, 0u, st));
     BandArgs b{};
     b.S = S;
     b.offsets = p->offsets;
@@ -334,37 +385,20 @@ int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, cons
     f.W_star = W_star;
     f.m_at_star = m_at_star;
     f.flags = ctx->flags;
+    f.need = rb.need;
+    f.any = rb.any;
     HIPCHK(launch_finalize(f, st));
+
+    // Where the band did not settle the optimum (it overflowed, or the optimum sat
+    // near its edge), the exact table of that (e, c) decides.  The kernels do
+    // nothing unless some (e, c) needs it.
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, rb.qb.B, rb.qb.part, rb.qb.hist, st, rb.any));
+    HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, k_max,
+                              rb.qb.hist, p->S, E, p->C, p->K, p->M, rb.cnt, rb.sum, rb.Wt, rb.mt,
+                              k_star, W_star, m_at_star, st, rb.need, rb.any));
     return DRO_OK;
 }
 
-long long max_segment(const dro_problem *p)
-{
-    long long max_seg = 0;
-    for (int s = 0; s < p->S; ++s)
-        max_seg = std::max(max_seg, (long long)(p->offsets_h[s + 1] - p->offsets_h[s]));
-    return max_seg;
-}
-
-struct QuantBufs {
-    uint32_t *hist, *part;
-    int B;
-};
-
-size_t quantile_bytes(const dro_problem *p, int num_cu)
-{
-    const int B = hist_parts(p->S, max_segment(p), num_cu);
-    return rup((size_t)p->S * kHistBins * 4) + (B > 1 ? rup((size_t)p->S * B * kHistBins * 4) : 0);
-}
-
-QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
-{
-    QuantBufs q;
-    q.B = hist_parts(p->S, max_segment(p), num_cu);
-    q.hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
-    q.part = q.B > 1 ? ar.take<uint32_t>((size_t)p->S * q.B * kHistBins) : nullptr;
-    return q;
-}
 
 int run_quantile(dro_ctx *ctx, const dro_problem *p, const QuantBufs &qb, int32_t *q_value,
                  int64_t *q_rank, hipStream_t st)
@@ -564,14 +598,14 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     hipStream_t st = (hipStream_t)stream;
     const int EC = E * p->C;
     const int P = refine_slices(sh.max_n);
-    rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(EC, P, p->K), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(p, EC, P, ctx->num_cu), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    RefineBufs rb = take_refine(ar, EC, P, p->K);
+    RefineBufs rb = take_refine(ar, p, EC, P, ctx->num_cu);
     return run_argmin(ctx, p, E, eps, S, k_max, 0, -1, rb, P, k_star, W_star, m_at_star, st);
 }
 
@@ -740,7 +774,8 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const int P = refine_slices(sh.max_n);
     const size_t need = dense_bytes(p, pl, true) + quantile_bytes(p, ctx->num_cu) +
-                        refine_bytes(C, P, p->K) + rup((size_t)C * 8) + 3 * rup((size_t)C * 4);
+                        refine_bytes(p, C, P, ctx->num_cu) + rup((size_t)C * 8) +
+                        3 * rup((size_t)C * 4);
     rc = ensure_ws(ctx, stage_bytes(p) + need, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
@@ -752,7 +787,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     double *S = ar.take<double>(ckm);
     double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
-    RefineBufs rb = take_refine(ar, C, P, p->K);
+    RefineBufs rb = take_refine(ar, p, C, P, ctx->num_cu);
     int64_t *q_rank = ar.take<int64_t>(C);
     int32_t *kmax = ar.take<int32_t>(C);
     int32_t *kcur = ar.take<int32_t>(C);

@@ -108,6 +108,8 @@ struct FinalArgs {
     double *W_star;
     int32_t *m_at_star;
     uint32_t *flags;
+    int32_t *need;   // [EC] 1 where the band did not settle the optimum (may be null)
+    uint32_t *any;   // set to 1 when some need[ec] is 1
 };
 hipError_t launch_finalize(const FinalArgs &a, hipStream_t st);
 
@@ -118,21 +120,26 @@ hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 hipError_t hist_prepare();
 // blocks per segment for the histogram pass
 int hist_parts(int S, long long max_seg, int num_cu);
-// hist: [S][kHistBins]; part: [S][B][kHistBins] scratch (unused when B == 1)
+// hist: [S][kHistBins]; part: [S][B][kHistBins] scratch (unused when B == 1).
+// With a gate, the kernels do nothing while *gate is 0.
 hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
-                            uint32_t *part, uint32_t *hist, hipStream_t st);
+                            uint32_t *part, uint32_t *hist, hipStream_t st,
+                            const uint32_t *gate = nullptr);
 hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st);
 
 // ---- exact table (value counts and prefix sums) -------------------------------
-// cnt: [S][kHistBins] u32, sum: [S][kHistBins] u64 scratch; k_star == null skips the argmin
+// cnt: [S][kHistBins] u32, sum: [S][kHistBins] u64 scratch; k_star == null skips the argmin.
+// With need ([E*C]), only the rows with need[e*C + c] != 0 are computed and only
+// their k_star, W_star, m_at_star written; with a gate, nothing runs while *gate is 0.
 hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const int32_t *L,
                               const int32_t *eta, const float *lam, const float *c_p,
                               const float *c_w, const float *eps, const int32_t *k_max,
                               const uint32_t *hist, int S, int E, int C, int K, int M,
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
-                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st);
+                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st,
+                              const int32_t *need = nullptr, const uint32_t *gate = nullptr);
 
 // continuous-multiplier dual over the same prefix counts (gamma: the smallest minimiser)
 hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, const int32_t *L,

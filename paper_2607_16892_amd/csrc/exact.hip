@@ -301,10 +301,17 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalArgs a)
         a.k_star[ec] = key / a.M;
         a.W_star[ec] = sJ[0];
         if (a.m_at_star) a.m_at_star[ec] = key % a.M;
-        // the exact optimum must sit well inside the screening band
+        // the exact optimum must sit well inside the screening band, and the band
+        // must have fitted; otherwise the exact table of this (e, c) decides
         const double T = a.thresh[ec];
-        if (!(sJ[0] * (1.0 + 0.5 * kBandTau) < T) || cnt == 0) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_MARGIN);
-        if (raw > kBandCap) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_FULL);
+        const bool margin = !(sJ[0] * (1.0 + 0.5 * kBandTau) < T) || cnt == 0;
+        const bool full = raw > kBandCap;
+        if (margin) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_MARGIN);
+        if (full) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_FULL);
+        if (a.need) {
+            a.need[ec] = (margin || full) ? 1 : 0;
+            if (margin || full) atomicOr(a.any, 1u);
+        }
     }
 }
 
@@ -333,9 +340,11 @@ constexpr int kHistThreads = 1024;
 
 __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *offsets,
                                                                  const int32_t *xi, int B,
-                                                                 uint32_t *part)
+                                                                 uint32_t *part,
+                                                                 const uint32_t *gate)
 {
     extern __shared__ uint32_t h[];  // kHistBins words
+    if (gate && *gate == 0u) return;
     const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
     const long long n0 = offsets[s], N = offsets[s + 1] - n0;
     const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
@@ -376,8 +385,10 @@ __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *
 }
 
 // hist[s][v] = sum over b of part[s][b][v]
-__global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t *hist)
+__global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t *hist,
+                                   const uint32_t *gate)
 {
+    if (gate && *gate == 0u) return;
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (long long)S * kHistBins) return;
     const long long s = i / kHistBins, v = i % kHistBins;
@@ -403,16 +414,16 @@ int hist_parts(int S, long long max_seg, int num_cu)
 }
 
 hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
-                            uint32_t *part, uint32_t *hist, hipStream_t st)
+                            uint32_t *part, uint32_t *hist, hipStream_t st, const uint32_t *gate)
 {
     if (S <= 0) return hipSuccess;
     uint32_t *dst = B == 1 ? hist : part;
     hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((long long)S * B)), dim3(kHistThreads),
-                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, dst);
+                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, dst, gate);
     if (B > 1) {
         const long long n = (long long)S * kHistBins;
         hipLaunchKernelGGL(hist_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                           (const uint32_t *)part, S, B, hist);
+                           (const uint32_t *)part, S, B, hist, gate);
     }
     return hipGetLastError();
 }
@@ -674,10 +685,11 @@ constexpr int kPrefixPer = kPrefixChunk / kPrefixThreads;  // 16
 __device__ __forceinline__ int pad32(int j) { return j + (j >> 5); }
 
 __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *hist, uint32_t *cnt,
-                                                                uint64_t *sum)
+                                                                uint64_t *sum, const uint32_t *gate)
 {
     __shared__ uint32_t hc[kPrefixChunk + kPrefixChunk / 32];
     __shared__ uint64_t rc[kPrefixThreads], rs[kPrefixThreads];
+    if (gate && *gate == 0u) return;
     constexpr int kChunks = (kHistBins + kPrefixChunk - 1) / kPrefixChunk;
     const int ch = (int)(blockIdx.x % kChunks), s = (int)(blockIdx.x / kChunks), t = threadIdx.x;
     const uint32_t *h = hist + (long long)s * kHistBins;
@@ -736,11 +748,12 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *
     }
 }
 
-hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st)
+hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
+                         const uint32_t *gate = nullptr)
 {
     const long long blocks = (long long)S * ((kHistBins + kPrefixChunk - 1) / kPrefixChunk);
     hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st, hist,
-                       cnt, sum);
+                       cnt, sum, gate);
     return hipGetLastError();
 }
 
@@ -762,12 +775,19 @@ constexpr int kTableThreads = 256;
 __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
     const float *lam, const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt,
-    const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star)
+    const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star,
+    const int32_t *need, const uint32_t *gate)
 {
     __shared__ double rv[8][kTableThreads];
     __shared__ int rm[8][kTableThreads];
     const long long ck = blockIdx.x;
     const int c = (int)(ck / K), k = (int)(ck % K), t = threadIdx.x;
+    if (gate && *gate == 0u) return;
+    if (need) {  // only the classes some radius row of which needs the table
+        bool any = false;
+        for (int e = 0; e < E; ++e) any = any || need[(long long)e * C + c] != 0;
+        if (!any) return;
+    }
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
     const int64_t L = L_[c], eta = eta_[k];
@@ -848,9 +868,12 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
 __global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, const int32_t *m_star,
                                                            const int32_t *k_max, int C, int K,
                                                            int32_t *k_star, double *W_star,
-                                                           int32_t *m_at_star)
+                                                           int32_t *m_at_star, const int32_t *need,
+                                                           const uint32_t *gate)
 {
     const int ec = blockIdx.x, c = ec % C, t = threadIdx.x;
+    if (gate && *gate == 0u) return;
+    if (need && need[ec] == 0) return;
     int kmax = K - 1;
     if (k_max) {
         kmax = k_max[c];
@@ -892,16 +915,18 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
                               const float *c_w, const float *eps, const int32_t *k_max,
                               const uint32_t *hist, int S, int E, int C, int K, int M,
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
-                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
+                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st,
+                              const int32_t *need, const uint32_t *gate)
 {
-    HIPRET(launch_prefix(hist, S, cnt, sum, st));
+    HIPRET(launch_prefix(hist, S, cnt, sum, st, gate));
     const long long n = (long long)C * K;
     hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)n), dim3(kTableThreads), 0, st, offsets,
                        seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,
-                       (const uint64_t *)sum, E, C, K, M, W, m_star);
+                       (const uint64_t *)sum, E, C, K, M, W, m_star, need, gate);
     if (k_star)
         hipLaunchKernelGGL(table_argmin_kernel, dim3(E * C), dim3(256), 0, st, (const double *)W,
-                           (const int32_t *)m_star, k_max, C, K, k_star, W_star, m_at_star);
+                           (const int32_t *)m_star, k_max, C, K, k_star, W_star, m_at_star, need,
+                           gate);
     return hipGetLastError();
 }
 
