@@ -541,7 +541,7 @@ int dro_validate(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps
     // min / max of every segment on the device
     int32_t *dmn = nullptr;
     HIPCHK(hipMalloc(&dmn, sizeof(int32_t) * 2 * S));
-    hipError_t e1 = launch_seg_minmax(p->offsets, p->xi, S, dmn, dmn + S, st);
+    hipError_t e1 = launch_seg_minmax(p->offsets, p->xi, S, max_segment(p), dmn, dmn + S, st);
     hipError_t e2 = e1 == hipSuccess ? hipStreamSynchronize(st) : e1;
     hipError_t e3 = e2 == hipSuccess ? hipMemcpy(mn.data(), dmn, 4 * S, hipMemcpyDeviceToHost) : e2;
     hipError_t e4 = e3 == hipSuccess ? hipMemcpy(mx.data(), dmn + S, 4 * S, hipMemcpyDeviceToHost) : e3;

@@ -218,7 +218,7 @@ hipError_t launch_state_objective(const SvcArgs &s, const double *T, const doubl
                                   int32_t *pre_route, double *out, hipStream_t st);
 
 // ---- validation ----------------------------------------------------------------
-hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, int32_t *mn,
-                             int32_t *mx, hipStream_t st);
+hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, long long max_seg,
+                             int32_t *mn, int32_t *mx, hipStream_t st);
 
 }  // namespace dro

@@ -622,19 +622,24 @@ hipError_t launch_bcd_finish(const int32_t *eta, int C, int K, int G, const floa
 }
 
 // ------------------------------------------------------------ validation ----
+// Block (segment s, part b of B): the smallest and largest sample of its share
+// of the segment, merged into mn[s] / mx[s] with atomic min / max (which the
+// caller sets to INT_MAX / INT_MIN first); the result does not depend on order.
 __global__ __launch_bounds__(256) void seg_minmax_kernel(const int64_t *offsets, const int32_t *xi,
-                                                         int32_t *mn, int32_t *mx)
+                                                         int B, int32_t *mn, int32_t *mx)
 {
-    const int s = blockIdx.x, t = threadIdx.x;
-    int a = 0x7fffffff, b = -0x7fffffff - 1;
-    for (long long n = offsets[s] + t; n < offsets[s + 1]; n += 256) {
+    const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B), t = threadIdx.x;
+    const long long n0 = offsets[s], N = offsets[s + 1] - n0;
+    const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
+    int a = 0x7fffffff, c = -0x7fffffff - 1;
+    for (long long n = lo + t; n < hi; n += 256) {
         const int v = xi[n];
         a = v < a ? v : a;
-        b = v > b ? v : b;
+        c = v > c ? v : c;
     }
     __shared__ int sa[256], sb[256];
     sa[t] = a;
-    sb[t] = b;
+    sb[t] = c;
     __syncthreads();
     for (int w = 128; w > 0; w >>= 1) {
         if (t < w) {
@@ -643,16 +648,21 @@ __global__ __launch_bounds__(256) void seg_minmax_kernel(const int64_t *offsets,
         }
         __syncthreads();
     }
-    if (t == 0) {
-        mn[s] = sa[0];
-        mx[s] = sb[0];
+    if (t == 0 && hi > lo) {
+        atomicMin(&mn[s], sa[0]);
+        atomicMax(&mx[s], sb[0]);
     }
 }
 
-hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, int32_t *mn,
-                             int32_t *mx, hipStream_t st)
+hipError_t launch_seg_minmax(const int64_t *offsets, const int32_t *xi, int S, long long max_seg,
+                             int32_t *mn, int32_t *mx, hipStream_t st)
 {
-    hipLaunchKernelGGL(seg_minmax_kernel, dim3(S), dim3(256), 0, st, offsets, xi, mn, mx);
+    // about 16K samples per block, at most 4096 blocks in all
+    const long long B = std::max(1LL, std::min(std::max(1LL, 4096LL / S), (max_seg + 16383) / 16384));
+    HIPRET(launch_fill_u32(reinterpret_cast<uint32_t *>(mn), S, 0x7fffffffu, st));
+    HIPRET(launch_fill_u32(reinterpret_cast<uint32_t *>(mx), S, 0x80000000u, st));
+    hipLaunchKernelGGL(seg_minmax_kernel, dim3((unsigned)(S * B)), dim3(256), 0, st, offsets, xi,
+                       (int)B, mn, mx);
     return hipGetLastError();
 }
 
