@@ -125,6 +125,8 @@ def bench_bcd(ctx, dev, iters: int):
         e1.record()
         torch.cuda.synchronize()
         times.append(e0.elapsed_time(e1))
+        if (it + 1) % 10 == 0:
+            _log(f"block step iteration {it + 1}/{iters}: {times[-1]:.1f} ms")
         k = o["k_next"]
         usage = o["usage"].cpu().numpy()
         binding = int((usage > 0.98 * w.groups.cap).sum())
