@@ -292,8 +292,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the work shards over classes with no exchange; see DESIGN.md). Use --gpus 1.",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(the work shards over classes with no exchange). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
