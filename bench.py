@@ -276,8 +276,8 @@ def _platform(dev) -> dict:
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mixture-16x1M")
     ap.add_argument("--cpu-samples", type=int, default=81920)
     ap.add_argument("--no-cpu-baseline", action="store_true")
