@@ -41,10 +41,10 @@ VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 
 # stripped, identified by the hash prefix) and are
 # reported as null for any other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "9a9f7ae608d0f09a",
+    "dense_code_sha256_16": "cabffb7d42a45ffc",
     "workload": "mixture-16x1M",
     "valu_instr_per_eval": 2.0597,       # SQ_INSTS_VALU x 64 / evaluations
-    "hbm_bytes_per_launch": 1638327.5 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
+    "hbm_bytes_per_launch": 1638297.24 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
     "source": "profiles/dense_kernel_mixture-16x1M_counters.md",
 }
 

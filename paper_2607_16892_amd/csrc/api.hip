@@ -139,7 +139,7 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
 }
 
 // Tiles of kTK x kTM pairs per lane; the samples of a class are split into P
-// slices of at least 1024 samples (P <= 64), each handled by its own blocks,
+// slices of at least kMinSlice samples (P <= 64), each handled by its own blocks,
 // whose partial sums of S a reduce kernel adds in a fixed order.  P is the
 // smallest whose grid fills its last wave of resident blocks (CUs x blocks
 // per CU) to at least 97 % and runs at least kMinWaves such waves; failing
@@ -152,6 +152,7 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
 // copied into the workspace at the start of every call, so device data that
 // disagrees with the host copies can never steer a kernel outside xi.
 constexpr long long kMinWaves = 32;
+constexpr long long kMinSlice = 64;
 constexpr long long kPartialBytes = 2LL << 30;
 
 size_t stage_bytes(const dro_problem *p)
@@ -185,7 +186,7 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     const long long base = (long long)C * pl.tiles_k * pl.tiles_m;
     const long long cap = (long long)num_cu * std::max(bpc, 1);
     const long long ckm_bytes = (long long)C * K * M * (long long)sizeof(double);
-    long long maxP = std::max(1LL, std::min(64LL, max_n / 1024));
+    long long maxP = std::max(1LL, std::min(64LL, max_n / kMinSlice));
     maxP = std::max(1LL, std::min(maxP, kPartialBytes / std::max(1LL, ckm_bytes)));
     long long fillP = 1, wellP = 0;
     double best = -1.0;
