@@ -30,7 +30,8 @@
  * J is then a fully specified double expression of the exact S:
  *   J = RN(RN(lam*eps) + RN(RN(S)/N)), round-to-nearest-even, no contraction.
  *
- * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared (see oracle/build.py).
+ * Build: gcc -O2 -std=gnu11 -fopenmp -ffp-contract=off -fno-fast-math -fPIC -shared
+ *        (the build() function of oracle/__init__.py).
  */
 #include <stdint.h>
 #include <stdlib.h>
