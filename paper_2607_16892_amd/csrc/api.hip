@@ -138,8 +138,10 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
     return DRO_OK;
 }
 
-// Tiles of kTK x kTM pairs per lane; the samples of a class are split into P
-// slices of at least kMinSlice samples (P <= 64), each handled by its own blocks,
+// Tiles of kTK x kTM pairs per lane; the samples of every class are split into
+// the same P slices (P <= 64, and the largest class's slices hold at least
+// kMinSlice samples; a smaller class's may be short or empty, which adds zero),
+// each handled by its own blocks,
 // whose partial sums of S a reduce kernel adds in a fixed order.  P is the
 // smallest whose grid fills its last wave of resident blocks (CUs x blocks
 // per CU) to at least 97 % and runs at least kMinWaves such waves; failing

@@ -87,6 +87,7 @@ RANDOM_CASES = [
     dict(seed=8, C=3, N=(2049, 1025, 4097), L=4096, K=513, M=70, E=1,
          cost_choices=[(4.0, 1.0), (8.0, 1.0), (2.0, 2.0)]),               # q N integer: ties
     dict(seed=10, C=6, N=(700, 33, 1500), alias=True, L=2000, K=97, M=40, E=19),  # 19 radii
+    dict(seed=11, C=4, N=(256, 511, 512, 16385), L=3000, K=33, M=40, E=2),  # slice-floor sizes
 ]
 
 
