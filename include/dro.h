@@ -75,7 +75,7 @@ enum {
  * error: where the screening band did not settle it, the exact table of that
  * (e, c) did, and the result is the same exact optimum either way. */
 enum {
-    DRO_FLAG_BAND_FULL = 1u,   /* a screening band held more candidates than the refine keeps */
+    DRO_FLAG_BAND_FULL = 1u,   /* a screening band held more candidates than it keeps (256)   */
     DRO_FLAG_BAND_MARGIN = 2u  /* the exact optimum sat too close to the band edge            */
 };
 

@@ -210,8 +210,6 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     return pl;
 }
 
-int refine_slices(long long max_n) { return (int)std::min(256LL, std::max(1LL, max_n / 8192)); }
-
 // S (approximate) into `S`, using `part` when the plan splits samples.
 int run_dense(dro_ctx *ctx, const dro_problem *p, const Shape &sh, double *S, double *part,
               const DensePlan &pl, hipStream_t st)
@@ -273,13 +271,13 @@ QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
     return q;
 }
 
-// Scratch of the exact argmin: the screening band, the exact partial sums of
-// its candidates, and the exact table that settles any (e, c) whose band did
-// not (histogram, prefix counts and sums, and the [E*C][K] table).
+// Scratch of the exact argmin: the screening band, the segments' prefix counts
+// and sums (from which the exact S of each candidate, and the exact table of
+// any (e, c) whose band did not settle its optimum, are formed), the value
+// histogram they come from unless the caller has one, and the [E*C][K] table.
 struct RefineBufs {
     int32_t *cand, *count;
     double *thresh, *chunk_min;
-    uint64_t *part;
     int32_t *need;
     uint32_t *any;
     QuantBufs qb;
@@ -291,16 +289,16 @@ struct RefineBufs {
 
 size_t band_chunks(int K) { return (size_t)(K + kBandKC - 1) / kBandKC; }
 
-size_t refine_bytes(const dro_problem *p, int EC, int P, int num_cu)
+size_t refine_bytes(const dro_problem *p, int EC, int num_cu, bool with_hist)
 {
     const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
     return rup((size_t)EC * kBandCap * 4) + rup((size_t)EC * 4) + rup((size_t)EC * 8) +
-           rup((size_t)EC * band_chunks(p->K) * 8) + rup((size_t)EC * kBandCap * P * 16) +
-           rup((size_t)EC * 4) + rup(4) + quantile_bytes(p, num_cu) + rup(bins * 4) +
-           rup(bins * 8) + rup(eck * 8) + rup(eck * 4);
+           rup((size_t)EC * band_chunks(p->K) * 8) + rup((size_t)EC * 4) + rup(4) +
+           (with_hist ? quantile_bytes(p, num_cu) : 0) + rup(bins * 4) + rup(bins * 8) +
+           rup(eck * 8) + rup(eck * 4);
 }
 
-RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int P, int num_cu)
+RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int num_cu, bool with_hist)
 {
     RefineBufs r;
     const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
@@ -308,10 +306,9 @@ RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int P, int num_c
     r.count = ar.take<int32_t>(EC);
     r.thresh = ar.take<double>(EC);
     r.chunk_min = ar.take<double>((size_t)EC * band_chunks(p->K));
-    r.part = ar.take<uint64_t>((size_t)EC * kBandCap * P * 2);
     r.need = ar.take<int32_t>(EC);
     r.any = ar.take<uint32_t>(1);
-    r.qb = take_quantile(ar, p, num_cu);
+    r.qb = with_hist ? take_quantile(ar, p, num_cu) : QuantBufs{nullptr, nullptr, 0};
     r.cnt = ar.take<uint32_t>(bins);
     r.sum = ar.take<uint64_t>(bins);
     r.Wt = ar.take<double>(eck);
@@ -319,9 +316,18 @@ RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int P, int num_c
     return r;
 }
 
-// Screen, refine and finalize for all (e, c) (c_only < 0) or for one class.
+// Value histogram (into rb.qb) and prefix counts and sums of every segment.
+int run_prefix(dro_ctx *ctx, const dro_problem *p, const RefineBufs &rb, hipStream_t st)
+{
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, rb.qb.B, rb.qb.part, rb.qb.hist, st));
+    HIPCHK(launch_prefix(rb.qb.hist, p->S, rb.cnt, rb.sum, st));
+    return DRO_OK;
+}
+
+// Screen and finalize for all (e, c) (c_only < 0) or for one class, over the
+// prefix counts and sums already in rb.cnt, rb.sum.
 int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, const double *S,
-               const int32_t *k_max, int e_row, int c_only, const RefineBufs &rb, int P,
+               const int32_t *k_max, int e_row, int c_only, const RefineBufs &rb,
                int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
 {
     const int EC = E * p->C;
@@ -349,39 +355,23 @@ int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, cons
     b.flags = ctx->flags;
     HIPCHK(launch_band(b, rb.chunk_min, st));
 
-    RefineArgs r{};
-    r.offsets = p->offsets;
-    r.seg = p->seg;
-    r.xi = p->xi;
-    r.L = p->L;
-    r.eta = p->eta;
-    r.lam = p->lam;
-    r.c_p = p->c_p;
-    r.c_w = p->c_w;
-    r.cand = rb.cand;
-    r.count = rb.count;
-    r.C = p->C;
-    r.M = p->M;
-    r.EC = EC;
-    r.P = P;
-    r.e_row = e_row;
-    r.c_only = c_only;
-    r.part = rb.part;
-    HIPCHK(launch_refine(r, st));
-
     FinalArgs f{};
     f.offsets = p->offsets;
     f.seg = p->seg;
+    f.L = p->L;
+    f.eta = p->eta;
     f.lam = p->lam;
+    f.c_p = p->c_p;
+    f.c_w = p->c_w;
     f.eps = eps;
+    f.cnt = rb.cnt;
+    f.sum = rb.sum;
     f.cand = rb.cand;
     f.count = rb.count;
     f.thresh = rb.thresh;
-    f.part = rb.part;
     f.C = p->C;
     f.M = p->M;
     f.EC = EC;
-    f.P = P;
     f.e_row = e_row;
     f.c_only = c_only;
     f.k_star = k_star;
@@ -395,13 +385,11 @@ int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, cons
     // Where the band did not settle the optimum (it overflowed, or the optimum sat
     // near its edge), the exact table of that (e, c) decides.  The kernels do
     // nothing unless some (e, c) needs it.
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, rb.qb.B, rb.qb.part, rb.qb.hist, st, rb.any));
     HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, k_max,
-                              rb.qb.hist, p->S, E, p->C, p->K, p->M, rb.cnt, rb.sum, rb.Wt, rb.mt,
-                              k_star, W_star, m_at_star, st, rb.need, rb.any));
+                              nullptr, p->S, E, p->C, p->K, p->M, rb.cnt, rb.sum, rb.Wt, rb.mt,
+                              k_star, W_star, m_at_star, st, rb.need, rb.any, false));
     return DRO_OK;
 }
-
 
 int run_quantile(dro_ctx *ctx, const dro_problem *p, const QuantBufs &qb, int32_t *q_value,
                  int64_t *q_rank, hipStream_t st)
@@ -600,16 +588,17 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     DeviceGuard g(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     const int EC = E * p->C;
-    const int P = refine_slices(sh.max_n);
-    rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(p, EC, P, ctx->num_cu), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(p, EC, ctx->num_cu, true), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    RefineBufs rb = take_refine(ar, p, EC, P, ctx->num_cu);
-    return run_argmin(ctx, p, E, eps, S, k_max, 0, -1, rb, P, k_star, W_star, m_at_star, st);
+    RefineBufs rb = take_refine(ar, p, EC, ctx->num_cu, true);
+    rc = run_prefix(ctx, p, rb, st);
+    if (rc) return rc;
+    return run_argmin(ctx, p, E, eps, S, k_max, 0, -1, rb, k_star, W_star, m_at_star, st);
 }
 
 int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t *q_rank,
@@ -775,9 +764,8 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
-    const int P = refine_slices(sh.max_n);
     const size_t need = dense_bytes(p, pl, true) + quantile_bytes(p, ctx->num_cu) +
-                        refine_bytes(p, C, P, ctx->num_cu) + rup((size_t)C * 8) +
+                        refine_bytes(p, C, ctx->num_cu, false) + rup((size_t)C * 8) +
                         3 * rup((size_t)C * 4);
     rc = ensure_ws(ctx, stage_bytes(p) + need, st);
     if (rc) return rc;
@@ -790,20 +778,22 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     double *S = ar.take<double>(ckm);
     double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
-    RefineBufs rb = take_refine(ar, p, C, P, ctx->num_cu);
+    RefineBufs rb = take_refine(ar, p, C, ctx->num_cu, false);
     int64_t *q_rank = ar.take<int64_t>(C);
     int32_t *kmax = ar.take<int32_t>(C);
     int32_t *kcur = ar.take<int32_t>(C);
 
     rc = run_quantile(ctx, p, qb, out->q_value, q_rank, st);
     if (rc) return rc;
+    // the quantile's value histogram also gives the prefix counts and sums of the exact argmin
+    HIPCHK(launch_prefix(qb.hist, p->S, rb.cnt, rb.sum, st));
     rc = run_dense(ctx, p, sh, S, part, pl, st);
     if (rc) return rc;
     HIPCHK(hipMemcpyAsync(kcur, k_prev, sizeof(int32_t) * C, hipMemcpyDeviceToDevice, st));
     for (int c = 0; c < C; ++c) {
         HIPCHK(launch_bcd_kmax(p->eta, C, p->K, grp->G, grp->cap, grp->conc, grp->kappa, kcur, c,
                                kmax, out->feasible, st));
-        rc = run_argmin(ctx, p, 1, eps, S, kmax, 0, c, rb, P, kcur, out->W_star, nullptr, st);
+        rc = run_argmin(ctx, p, 1, eps, S, kmax, 0, c, rb, kcur, out->W_star, nullptr, st);
         if (rc) return rc;
     }
     HIPCHK(launch_bcd_finish(p->eta, C, p->K, grp->G, grp->conc, grp->kappa, kcur, out->usage,

@@ -76,33 +76,24 @@ struct BandArgs {
 // chunk_min: [EC][ceil(K / kBandKC)] scratch
 hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st);
 
-struct RefineArgs {
+// Exact S of each screened candidate from the prefix counts and sums of its
+// class's segment (cnt, sum: [S][kHistBins], from launch_prefix), its exact J,
+// and the lowest-index optimum of every (e, c).
+struct FinalArgs {
     const int64_t *offsets;
     const int32_t *seg;
-    const int32_t *xi;
     const int32_t *L;
     const int32_t *eta;
     const float *lam;
     const float *c_p;
     const float *c_w;
-    const int32_t *cand;
-    const int32_t *count;
-    int C, M, EC, P;
-    int e_row, c_only;
-    uint64_t *part;  // [EC][kBandCap][P][2] (lo, hi) exact partial sums
-};
-hipError_t launch_refine(const RefineArgs &a, hipStream_t st);
-
-struct FinalArgs {
-    const int64_t *offsets;
-    const int32_t *seg;
-    const float *lam;
     const float *eps;
+    const uint32_t *cnt;
+    const uint64_t *sum;
     const int32_t *cand;
     const int32_t *count;
     const double *thresh;
-    const uint64_t *part;
-    int C, M, EC, P;
+    int C, M, EC;
     int e_row, c_only;
     int32_t *k_star;
     double *W_star;
@@ -130,16 +121,22 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
                          int64_t *q_rank, hipStream_t st);
 
 // ---- exact table (value counts and prefix sums) -------------------------------
+// cnt[s][v] = #{x <= v}, sum[s][v] = sum of the samples <= v of segment s, from
+// its value histogram; with a gate, nothing runs while *gate is 0.
+hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
+                         const uint32_t *gate = nullptr);
 // cnt: [S][kHistBins] u32, sum: [S][kHistBins] u64 scratch; k_star == null skips the argmin.
 // With need ([E*C]), only the rows with need[e*C + c] != 0 are computed and only
 // their k_star, W_star, m_at_star written; with a gate, nothing runs while *gate is 0.
+// with_prefix = false takes cnt and sum as already formed from hist.
 hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const int32_t *L,
                               const int32_t *eta, const float *lam, const float *c_p,
                               const float *c_w, const float *eps, const int32_t *k_max,
                               const uint32_t *hist, int S, int E, int C, int K, int M,
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
                               int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st,
-                              const int32_t *need = nullptr, const uint32_t *gate = nullptr);
+                              const int32_t *need = nullptr, const uint32_t *gate = nullptr,
+                              bool with_prefix = true);
 
 // continuous-multiplier dual over the same prefix counts (gamma: the smallest minimiser)
 hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, const int32_t *L,

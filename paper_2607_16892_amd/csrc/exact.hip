@@ -70,6 +70,41 @@ __device__ __forceinline__ void add128(uint64_t &lo, uint64_t &hi, uint64_t blo,
     lo = r;
 }
 
+// floor(a / b) for b > 0 and |a| < 2^62: a double estimate (within 1 of the
+// quotient for the ranges used here) corrected with exact integer products.
+__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)
+{
+    int64_t q = (int64_t)floor((double)a / (double)b);
+    while (q * b > a) --q;
+    while ((q + 1) * b <= a) ++q;
+    return q;
+}
+
+// Exact S of one (class, grid point, multiplier), in units of 2^-33, from the
+// prefix counts cn[v] = #{x <= v} and sums sm[v] = sum{x : x <= v} of the
+// class's segment (N samples).  For 0 <= x, eta <= L the three candidates of
+// Step 4 reduce to the larger of two lines, B - a1 x and C - a2 (L - x) with
+// B = c_w eta, C = c_p (L - eta), a1 = min(g, c_w), a2 = min(g, c_p); the
+// first is the larger up to t = floor((B - C + a2 L) / (a1 + a2)), so
+//   S = B cnt(t) - a1 sum(t) + (C - a2 L)(N - cnt(t)) + a2 (sum_all - sum(t)),
+// every term an exact integer (the sum is non-negative, as phi is).
+__device__ __forceinline__ unsigned __int128 exact_S_prefix(const uint32_t *cn, const uint64_t *sm,
+                                                           int64_t N, int64_t L, int64_t eta,
+                                                           int64_t CP, int64_t CW, int64_t G)
+{
+    const int64_t B = CW * eta, Cc = CP * (L - eta);
+    const int64_t A1 = G < CW ? G : CW, A2 = G < CP ? G : CP;
+    const int64_t tmax = L < kHistBins - 1 ? L : kHistBins - 1;
+    int64_t tt = floor_div(B - Cc + A2 * L, A1 + A2);
+    tt = tt < -1 ? -1 : (tt > tmax ? tmax : tt);
+    const __int128 ct = tt >= 0 ? (__int128)cn[tt] : 0;
+    const __int128 st = tt >= 0 ? (__int128)sm[tt] : 0;
+    const __int128 sum_all = (__int128)sm[kHistBins - 1];
+    const __int128 S = (__int128)B * ct - (__int128)A1 * st + (__int128)(Cc - A2 * L) * ((__int128)N - ct) +
+                       (__int128)A2 * (sum_all - st);
+    return (unsigned __int128)S;
+}
+
 __global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
 {
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -196,85 +231,34 @@ hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st)
     return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- refine ----
-// Block (slice p, problem ec): exact partial sums of phi over slice p of the
-// class's samples, for every screened candidate of ec.
-__global__ __launch_bounds__(256) void refine_kernel(RefineArgs a)
-{
-    const int p = blockIdx.y;
-    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
-    const int c = ec % a.C;
-    const int t = threadIdx.x;
-    const int s = seg_of_x(a.seg, c);
-    const long long n0 = a.offsets[s], N = a.offsets[s + 1] - n0;
-    const long long lo = n0 + (N * p) / a.P, hi = n0 + (N * (p + 1)) / a.P;
-    const int64_t CP = fix33(a.c_p[c]), CW = fix33(a.c_w[c]);
-    const int64_t L = a.L[c];
-    const int cnt = min(a.count[ec], kBandCap);
-
-    __shared__ uint64_t s_lo[256], s_hi[256];
-    for (int i = 0; i < cnt; ++i) {
-        const int packed = a.cand[(long long)ec * kBandCap + i];
-        const int k = packed / a.M, m = packed % a.M;
-        const int64_t eta = a.eta[k];
-        const int64_t G = fix33(a.lam[m]);
-        uint64_t alo = 0, ahi = 0;
-        for (long long n = lo + t; n < hi; n += 256) {
-            const uint64_t v = (uint64_t)phi_fix(eta, a.xi[n], L, CP, CW, G);
-            add128(alo, ahi, v, 0);
-        }
-        s_lo[t] = alo;
-        s_hi[t] = ahi;
-        __syncthreads();
-        for (int w = 128; w > 0; w >>= 1) {
-            if (t < w) {
-                uint64_t l = s_lo[t], h = s_hi[t];
-                add128(l, h, s_lo[t + w], s_hi[t + w]);
-                s_lo[t] = l;
-                s_hi[t] = h;
-            }
-            __syncthreads();
-        }
-        if (t == 0) {
-            uint64_t *o = a.part + (((long long)ec * kBandCap + i) * a.P + p) * 2;
-            o[0] = s_lo[0];
-            o[1] = s_hi[0];
-        }
-        __syncthreads();
-    }
-}
-
-hipError_t launch_refine(const RefineArgs &a, hipStream_t st)
-{
-    const int xs = a.c_only >= 0 ? 1 : a.EC;
-    hipLaunchKernelGGL(refine_kernel, dim3(xs, a.P), dim3(256), 0, st, a);
-    return hipGetLastError();
-}
-
 // -------------------------------------------------------------- finalize ----
-// Block per ec: exact S and J of every candidate, then the lowest (k, m) with
-// the smallest J (candidates are packed k * M + m, so one integer orders them).
+// Block per ec: the exact S of every screened candidate from the segment's
+// prefix counts and sums, its exact J, then the lowest (k, m) with the
+// smallest J (candidates are packed k * M + m, so one integer orders them).
 __global__ __launch_bounds__(256) void finalize_kernel(FinalArgs a)
 {
     const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
     const int e = ec / a.C, c = ec % a.C;
     const int t = threadIdx.x;
     const int s = seg_of_x(a.seg, c);
-    const double N = (double)(a.offsets[s + 1] - a.offsets[s]);
+    const int64_t Ni = a.offsets[s + 1] - a.offsets[s];
+    const double N = (double)Ni;
     const double ev = (double)a.eps[(long long)e * a.C + c];
+    const int64_t L = a.L[c];
+    const int64_t CP = fix33(a.c_p[c]), CW = fix33(a.c_w[c]);
+    const uint32_t *cn = a.cnt + (long long)s * kHistBins;
+    const uint64_t *sm = a.sum + (long long)s * kHistBins;
     const int raw = a.count[ec];
     const int cnt = min(raw, kBandCap);
 
     double bJ = __builtin_inf();
     int bkey = 0x7fffffff;
     for (int i = t; i < cnt; i += 256) {
-        uint64_t lo = 0, hi = 0;
-        const uint64_t *pp = a.part + ((long long)ec * kBandCap + i) * a.P * 2;
-        for (int p = 0; p < a.P; ++p) add128(lo, hi, pp[2 * p], pp[2 * p + 1]);
         const int key = a.cand[(long long)ec * kBandCap + i];
-        const int m = key % a.M;
+        const int k = key / a.M, m = key % a.M;
+        const unsigned __int128 S = exact_S_prefix(cn, sm, Ni, L, a.eta[k], CP, CW, fix33(a.lam[m]));
         const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
-                                   __ddiv_rn(fix128_to_double(lo, hi), N));
+                                   __ddiv_rn(fix128_to_double((uint64_t)S, (uint64_t)(S >> 64)), N));
         if (J < bJ || (J == bJ && key < bkey)) {
             bJ = J;
             bkey = key;
@@ -759,22 +743,12 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *
 }
 
 hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
-                         const uint32_t *gate = nullptr)
+                         const uint32_t *gate)
 {
     const long long blocks = (long long)S * ((kHistBins + kPrefixChunk - 1) / kPrefixChunk);
     hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st, hist,
                        cnt, sum, gate);
     return hipGetLastError();
-}
-
-// floor(a / b) for b > 0 and |a| < 2^62: a double estimate (within 1 of the
-// quotient for the ranges used here) corrected with exact integer products.
-__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)
-{
-    int64_t q = (int64_t)floor((double)a / (double)b);
-    while (q * b > a) --q;
-    while ((q + 1) * b <= a) ++q;
-    return q;
 }
 
 // Block per (c, k), thread per multiplier (m = t, t + 256, ...): exact S,
@@ -803,10 +777,7 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     const int64_t L = L_[c], eta = eta_[k];
     const uint32_t *cn = cnt + (long long)s * kHistBins;
     const uint64_t *sm = sum + (long long)s * kHistBins;
-    const __int128 sum_all = (__int128)sm[kHistBins - 1];
-    const int64_t tmax = L < kHistBins - 1 ? L : kHistBins - 1;
     const int64_t CP = fix33(c_p[c]), CW = fix33(c_w[c]);
-    const int64_t B = CW * eta, Cc = CP * (L - eta);
     const double Nd = (double)N;
     for (int e0 = 0; e0 < E; e0 += 8) {
         double best[8];
@@ -819,17 +790,7 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
             ev[q] = (e0 + q < E) ? (double)eps[(long long)(e0 + q) * C + c] : 0.0;
         }
         for (int m = t; m < M; m += kTableThreads) {
-            const int64_t G = fix33(lam[m]);
-            const int64_t A1 = G < CW ? G : CW, A2 = G < CP ? G : CP;
-            const int64_t num = B - Cc + A2 * L;
-            int64_t tt = floor_div(num, A1 + A2);
-            tt = tt < -1 ? -1 : (tt > tmax ? tmax : tt);
-            const __int128 ct = tt >= 0 ? (__int128)cn[tt] : 0;
-            const __int128 st = tt >= 0 ? (__int128)sm[tt] : 0;
-            const __int128 S = (__int128)B * ct - (__int128)A1 * st +
-                               (__int128)(Cc - A2 * L) * ((__int128)N - ct) +
-                               (__int128)A2 * (sum_all - st);
-            const unsigned __int128 u = (unsigned __int128)S;
+            const unsigned __int128 u = exact_S_prefix(cn, sm, N, L, eta, CP, CW, fix33(lam[m]));
             const double q_ = __ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), Nd);
             const double lm = (double)lam[m];
             const int nq = E - e0;
@@ -926,9 +887,9 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
                               const uint32_t *hist, int S, int E, int C, int K, int M,
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
                               int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st,
-                              const int32_t *need, const uint32_t *gate)
+                              const int32_t *need, const uint32_t *gate, bool with_prefix)
 {
-    HIPRET(launch_prefix(hist, S, cnt, sum, st, gate));
+    if (with_prefix) HIPRET(launch_prefix(hist, S, cnt, sum, st, gate));
     const long long n = (long long)C * K;
     hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)n), dim3(kTableThreads), 0, st, offsets,
                        seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,
