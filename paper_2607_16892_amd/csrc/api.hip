@@ -62,6 +62,12 @@ struct DeviceGuard {
     }
 };
 
+// Makes ctx's device current for the rest of the calling entry point, or
+// returns DRO_EHIP from it when the device cannot be selected.
+#define ENTER_DEVICE(ctx)                                                                   \
+    DeviceGuard guard_((ctx)->device);                                                      \
+    if (!guard_.ok) return fail((ctx), DRO_EHIP, "cannot select device %d", (ctx)->device)
+
 // Bump allocator over the context workspace.
 struct Arena {
     char *base = nullptr;
@@ -428,9 +434,10 @@ int dro_create(int hip_device, dro_ctx **out)
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || hip_device < 0 || hip_device >= n)
         return DRO_EINVAL;
+    DeviceGuard g(hip_device);
+    if (!g.ok) return DRO_EHIP;
     dro_ctx *ctx = new dro_ctx();
     ctx->device = hip_device;
-    DeviceGuard g(hip_device);
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, hip_device) == hipSuccess && prop.multiProcessorCount > 0)
         ctx->num_cu = prop.multiProcessorCount;
@@ -440,10 +447,15 @@ int dro_create(int hip_device, dro_ctx **out)
         delete ctx;
         return DRO_EHIP;
     }
-    if (hipMalloc(&ctx->flags, sizeof(uint32_t)) != hipSuccess ||
-        hipMemset(ctx->flags, 0, sizeof(uint32_t)) != hipSuccess) {
+    if (hipMalloc(&ctx->flags, sizeof(uint32_t)) != hipSuccess) {
+        (void)hipGetLastError();
         delete ctx;
         return DRO_ENOMEM;
+    }
+    if (hipMemset(ctx->flags, 0, sizeof(uint32_t)) != hipSuccess) {
+        (void)hipFree(ctx->flags);
+        delete ctx;
+        return DRO_EHIP;
     }
     *out = ctx;
     return DRO_OK;
@@ -452,7 +464,7 @@ int dro_create(int hip_device, dro_ctx **out)
 void dro_destroy(dro_ctx *ctx)
 {
     if (!ctx) return;
-    DeviceGuard g(ctx->device);
+    DeviceGuard g(ctx->device);  // best effort: destroy returns nothing
     (void)hipDeviceSynchronize();
     if (ctx->ws) (void)hipFree(ctx->ws);
     if (ctx->flags) (void)hipFree(ctx->flags);
@@ -464,7 +476,7 @@ const char *dro_last_error(const dro_ctx *ctx) { return ctx ? ctx->err : "no con
 int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out)
 {
     if (!ctx || !flags_out) return fail(ctx, DRO_EINVAL, "NULL argument");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     HIPCHK(hipDeviceSynchronize());
     HIPCHK(hipMemcpy(flags_out, ctx->flags, sizeof(uint32_t), hipMemcpyDeviceToHost));
     HIPCHK(hipMemset(ctx->flags, 0, sizeof(uint32_t)));
@@ -478,7 +490,7 @@ int dro_validate(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps
     int rc = check_problem(ctx, p, &sh);
     if (rc) return rc;
     if (E < 0 || (E > 0 && !eps)) return fail(ctx, DRO_EINVAL, "bad radius arguments");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C, S = p->S, K = p->K, M = p->M;
     std::vector<int64_t> off(S + 1);
@@ -555,8 +567,7 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     int rc = check_problem(ctx, p, &sh);
     if (rc) return rc;
     if (E <= 0 || !eps || !W) return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W non-NULL");
-    DeviceGuard g(ctx->device);
-    if (!g.ok) return fail(ctx, DRO_EHIP, "cannot select device %d", ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     rc = ensure_ws(ctx, stage_bytes(p) + dense_bytes(p, pl, S == nullptr), st);
@@ -585,7 +596,7 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     if (rc) return rc;
     if (E <= 0 || !eps || !S || !k_star || !W_star)
         return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, S, k_star, W_star non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int EC = E * p->C;
     rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(p, EC, ctx->num_cu, true), st);
@@ -608,7 +619,7 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     int rc = check_problem(ctx, p, &sh);
     if (rc) return rc;
     if (!q_value || !q_rank) return fail(ctx, DRO_EINVAL, "q_value and q_rank must be non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu), st);
     if (rc) return rc;
@@ -630,7 +641,7 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     if (rc) return rc;
     if (E <= 0 || !eps || !W || !m_star || (k_star && !W_star))
         return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, m_star (and W_star with k_star) non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
     rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
@@ -658,7 +669,7 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     if (rc) return rc;
     if (E <= 0 || !eps || !W || !gamma)
         return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, gamma non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
     rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
@@ -685,7 +696,7 @@ int class_moments(dro_ctx *ctx, const dro_problem *p, int64_t *count, int64_t *s
     if (rc) return rc;
     if (!count || !sum || !sumsq || !xmax)
         return fail(ctx, DRO_EINVAL, "count, sum, sumsq and xmax must be non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu), st);
     if (rc) return rc;
@@ -710,7 +721,7 @@ int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const in
         return fail(ctx, DRO_EINVAL, "R must be > 0 and eta_r, cost, cover non-NULL");
     if ((long long)R * p->C > (1LL << 31))
         return fail(ctx, DRO_ELIMIT, "R*C = %lld reservations exceed 2^31", (long long)R * p->C);
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
     rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
@@ -735,7 +746,7 @@ int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t
     int rc = check_problem(ctx, p, &sh);
     if (rc) return rc;
     if (!k0) return fail(ctx, DRO_EINVAL, "k0 must be non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     rc = ensure_ws(ctx, stage_bytes(p) + rup((size_t)p->C * 8), st);
     if (rc) return rc;
@@ -760,7 +771,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
         return fail(ctx, DRO_EINVAL, "a block-step argument or output is NULL");
     if (grp->G <= 0 || !grp->cap || !grp->conc || !std::isfinite(grp->kappa) || grp->kappa < 0.0f)
         return fail(ctx, DRO_EINVAL, "groups need G > 0, cap, conc and a finite kappa >= 0");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
@@ -950,7 +961,7 @@ int bcd_service_times(dro_ctx *ctx, const dro_problem *p, const dro_service *svc
     rc = check_service(ctx, p->C, svc);
     if (rc) return rc;
     if (!T || !ET2) return fail(ctx, DRO_EINVAL, "T and ET2 must be non-NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
     rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + 4 * rup((size_t)C * 8), st);
@@ -978,7 +989,7 @@ int bcd_queue_state(dro_ctx *ctx, int32_t C, const dro_service *svc, const doubl
     if (rc) return rc;
     if (!T || !ET2 || !pi || !z || !eta_c || !delta || !Wq || !cap || !conc)
         return fail(ctx, DRO_EINVAL, "a queue-state argument is NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     HIPCHK(launch_state(svc_args(svc, C), T, ET2, pi, z, eta_c, delta, Wq, cap, conc, mem,
                         (hipStream_t)stream));
     return DRO_OK;
@@ -993,7 +1004,7 @@ int bcd_routing_lp(dro_ctx *ctx, int32_t C, const dro_service *svc, const double
     if (rc) return rc;
     if (!Wc || !T || !Wq || !z || !eta_c || !delta || !pi || !lp_objective || !info)
         return fail(ctx, DRO_EINVAL, "a routing-LP argument is NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int G = svc->G, m = 2 * C + G;
     rc = ensure_ws(ctx, rup(lp1_tableau_doubles(C, G) * 8) + rup((size_t)m * 4), st);
@@ -1016,7 +1027,7 @@ int bcd_reservation_sweep(dro_ctx *ctx, int32_t C, int32_t K, const double *W,
         return fail(ctx, DRO_EINVAL, "sweep needs C, K, G > 0 and non-NULL W, eta, conc, cap, k");
     if (!std::isfinite(kappa) || kappa < 0.0f) return fail(ctx, DRO_EINVAL, "kappa must be >= 0");
     if (k_in == k_out) return fail(ctx, DRO_EINVAL, "k_in and k_out must differ");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     HIPCHK(launch_sweep(W, eta, C, K, G, conc, cap, kappa, k_in, k_out, feasible,
                         (hipStream_t)stream));
     return DRO_OK;
@@ -1028,7 +1039,7 @@ int bcd_prefix_cache(dro_ctx *ctx, int32_t C, int32_t G, const double *conc, uin
     if (!ctx) return DRO_EINVAL;
     if (C <= 0 || G <= 0 || !conc || !delta)
         return fail(ctx, DRO_EINVAL, "prefix cache needs C, G > 0 and non-NULL conc, delta");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     HIPCHK(launch_cache(conc, C * G, delta, (hipStream_t)stream));
     return DRO_OK;
 }
@@ -1043,7 +1054,7 @@ int bcd_config_search(dro_ctx *ctx, int32_t C, const dro_service *svc, const dou
     if (rc) return rc;
     if (!Wc || !T || !ET2 || !pi || !eta_c || !delta || !z)
         return fail(ctx, DRO_EINVAL, "a configuration-search argument is NULL");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const long long nz = count_configs(ctx, svc, st);
     if (nz < 0) return fail(ctx, DRO_EHIP, "stream synchronisation failed");
@@ -1077,7 +1088,7 @@ int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dr
         return fail(ctx, DRO_EINVAL, "a solver argument is NULL");
     if (max_outer <= 0 || max_inner <= 0)
         return fail(ctx, DRO_EINVAL, "max_outer and max_inner must be positive");
-    DeviceGuard g(ctx->device);
+    ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C, G = svc->G, K = p->K, J = svc->J, CG = C * G, m = 2 * C + G;
     const long long nz = count_configs(ctx, svc, st);
