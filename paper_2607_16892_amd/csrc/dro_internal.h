@@ -107,7 +107,7 @@ hipError_t launch_finalize(const FinalArgs &a, hipStream_t st);
 // ---- quantile ----------------------------------------------------------------
 constexpr int kHistBins = 32769;   // values 0 .. 2^15
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st);
-// allows the histogram kernel its 128 KB of dynamic LDS (once per device)
+// allows the histogram and quantile-select kernels their 128 KB of dynamic LDS (once per device)
 hipError_t hist_prepare();
 // blocks per segment for the histogram pass
 int hist_parts(int S, long long max_seg, int num_cu);

@@ -382,11 +382,14 @@ __global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t 
     hist[i] = acc;
 }
 
+hipError_t select_prepare();
+
 hipError_t hist_prepare()
 {
-    return hipFuncSetAttribute(reinterpret_cast<const void *>(histogram_kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                               (int)(kHistBins * sizeof(uint32_t)));
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(histogram_kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)(kHistBins * sizeof(uint32_t)));
+    return e != hipSuccess ? e : select_prepare();
 }
 
 int hist_parts(int S, long long max_seg, int num_cu)
@@ -436,29 +439,40 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offs
                                                              const float *c_w, const uint32_t *hist,
                                                              int32_t *q_value, int64_t *q_rank)
 {
+    extern __shared__ uint32_t hl[];  // the segment's histogram, kHistBins words
+    __shared__ uint64_t sc[kSelThreads / 64];
     const int c = blockIdx.x, t = threadIdx.x;
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
-    const int64_t j = exact_rank(c_p[c], c_w[c], N);
     const uint32_t *h = hist + (long long)s * kHistBins;
+    for (int v = t; v < kHistBins; v += kSelThreads) hl[v] = h[v];  // coalesced
+    const int64_t j = exact_rank(c_p[c], c_w[c], N);
+    __syncthreads();
+    // thread t owns the bins [t * per, (t + 1) * per); per is odd, so a wave's
+    // LDS reads fall in distinct banks
     constexpr int per = (kHistBins + kSelThreads - 1) / kSelThreads;
     const int b0 = t * per, b1 = min(kHistBins, b0 + per);
     uint64_t part = 0;
-    for (int v = b0; v < b1; ++v) part += h[v];
-    __shared__ uint64_t sc[kSelThreads];
-    sc[t] = part;
-    __syncthreads();
-    for (int w = 1; w < kSelThreads; w <<= 1) {  // inclusive scan
-        const uint64_t add = t >= w ? sc[t - w] : 0;
-        __syncthreads();
-        sc[t] += add;
-        __syncthreads();
+    for (int v = b0; v < b1; ++v) part += hl[v];
+    // inclusive scan of the thread totals: within each wave by shuffles, then
+    // over the wave totals
+    const int lane = t & 63, wave = t >> 6;
+    uint64_t incl = part;
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t o = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += o;
     }
-    const uint64_t before = sc[t] - part;
-    if ((int64_t)before < j && j <= (int64_t)sc[t]) {
+    if (lane == 63) sc[wave] = incl;
+    __syncthreads();
+    if (t == 0)
+        for (int w = 1; w < kSelThreads / 64; ++w) sc[w] += sc[w - 1];
+    __syncthreads();
+    if (wave > 0) incl += sc[wave - 1];
+    const uint64_t before = incl - part;
+    if ((int64_t)before < j && j <= (int64_t)incl) {
         uint64_t cum = before;
         for (int v = b0; v < b1; ++v) {
-            cum += h[v];
+            cum += hl[v];
             if ((int64_t)cum >= j) {
                 q_value[c] = v;
                 break;
@@ -468,12 +482,19 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offs
     if (t == 0) q_rank[c] = j;
 }
 
+hipError_t select_prepare()
+{
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(select_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)(kHistBins * sizeof(uint32_t)));
+}
+
 hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st)
 {
-    hipLaunchKernelGGL(select_kernel, dim3(C), dim3(kSelThreads), 0, st, offsets, seg, c_p, c_w,
-                       hist, q_value, q_rank);
+    hipLaunchKernelGGL(select_kernel, dim3(C), dim3(kSelThreads), kHistBins * sizeof(uint32_t), st,
+                       offsets, seg, c_p, c_w, hist, q_value, q_rank);
     return hipGetLastError();
 }
 
