@@ -112,29 +112,42 @@ __global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
 }
 
 // ------------------------------------------------------------------ band ----
-// Screening, over (problem ec = e*C + c, chunk of kBandKC grid points):
-//   band_min:     the smallest approximate dual value J~ = lam eps + S~ / N of
-//                 the chunk's pairs (k <= kmax, m <= m_first);
-//   band_collect: threshold T = (1 + tau) min J~ + slack from the chunk minima,
-//                 then every pair with J~ <= T appended to the problem's list
-//                 through a global counter.  The list order is irrelevant: the
-//                 refine evaluates every listed pair exactly and keeps the
-//                 lowest (J, k, m).
+// Screening.  A block takes one class c, up to kBandE radius rows e of it and
+// one chunk of kBandKC grid points, and reads each S[c, k, m] of the chunk once
+// for all of its rows:
+//   band_min:     per row, the smallest approximate dual value J~ = lam eps + S~ / N
+//                 of the chunk's pairs (k <= kmax, m <= m_first);
+//   band_collect: per row, the threshold T = (1 + tau) min J~ + slack from the
+//                 chunk minima, then every pair with J~ <= T appended to the row's
+//                 list through a global counter.  The list order is irrelevant: the
+//                 finalize evaluates every listed pair exactly and keeps the lowest
+//                 (J, k, m).
 // For lam_m >= max(c_p, c_w) every sample keeps its own point, so S is the SAA
 // sum for all such m and J can only grow with m: only the first of them
 // (m_first) can be a lowest-index minimiser, and the others are not screened.
-struct BandProblem {
-    int ec, c, kmax, mlim;
-    double ninv, ev, slack;
+constexpr int kBandE = 8;  // radius rows per block (one when the call has a single row)
+
+template <int R>
+struct BandGroup {
+    int c, e0, ne, kmax, mlim;
+    double ninv, slack;
+    double ev[R];
 };
 
-__device__ BandProblem band_problem(const BandArgs &a, int ec)
+template <int R>
+__device__ BandGroup<R> band_group(const BandArgs &a)
 {
     __shared__ int s_mf;
-    BandProblem q;
-    q.ec = ec;
-    q.c = ec % a.C;
-    const int e = ec / a.C;
+    BandGroup<R> q;
+    if (a.c_only >= 0) {
+        q.c = a.c_only;
+        q.e0 = a.e_row;
+        q.ne = 1;
+    } else {
+        q.c = (int)(blockIdx.x % a.C);
+        q.e0 = (int)(blockIdx.x / a.C) * R;
+        q.ne = min(R, a.E - q.e0);
+    }
     const float cp = a.c_p[q.c], cw = a.c_w[q.c];
     const float top = cp > cw ? cp : cw;
     if (threadIdx.x == 0) s_mf = a.M - 1;
@@ -150,72 +163,119 @@ __device__ BandProblem band_problem(const BandArgs &a, int ec)
     }
     const int s = seg_of_x(a.seg, q.c);
     q.ninv = 1.0 / (double)(a.offsets[s + 1] - a.offsets[s]);
-    q.ev = (double)a.eps[(long long)e * a.C + q.c];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        q.ev[r] = r < q.ne ? (double)a.eps[(long long)(q.e0 + r) * a.C + q.c] : 0.0;
     q.slack = 1e-12 * (double)(cp + cw) * (double)a.L[q.c];
     return q;
 }
 
-__device__ __forceinline__ double approx_J(const BandArgs &a, const BandProblem &q, int k, int m)
+// Minimum over the 256-thread block of each of v[0..n): shuffles inside each
+// wave, then the four wave results through LDS.  Every thread gets them.
+template <int R>
+__device__ void block_min_rows(double (&v)[R], int n)
 {
-    return (double)a.lam[m] * q.ev + a.S[((long long)q.c * a.K + k) * a.M + m] * q.ninv;
-}
-
-__device__ double block_min(double v)
-{
-    __shared__ double sm[256];
-    const int t = threadIdx.x;
-    sm[t] = v;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (t < w) sm[t] = sm[t + w] < sm[t] ? sm[t + w] : sm[t];
-        __syncthreads();
+    __shared__ double sm[4][R];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (r >= n) break;
+        double x = v[r];
+        for (int d = 32; d > 0; d >>= 1) {
+            const double o = __shfl_xor(x, d, 64);
+            x = o < x ? o : x;
+        }
+        if (lane == 0) sm[wave][r] = x;
     }
-    const double r = sm[0];
     __syncthreads();
-    return r;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (r >= n) break;
+        double x = sm[0][r];
+        for (int w = 1; w < 4; ++w) x = sm[w][r] < x ? sm[w][r] : x;
+        v[r] = x;
+    }
+    __syncthreads();
 }
 
+template <int R>
 __global__ __launch_bounds__(256) void band_min_kernel(BandArgs a, double *chunk_min, int nchunks)
 {
-    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
-    const BandProblem q = band_problem(a, ec);
+    const BandGroup<R> q = band_group<R>(a);
     const int k0 = blockIdx.y * kBandKC;
     const int k1 = min(k0 + kBandKC - 1, q.kmax);
     const int nm = q.mlim + 1;
     const int npair = k1 >= k0 ? (k1 - k0 + 1) * nm : 0;
-    double lmin = __builtin_inf();
+    double lmin[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) lmin[r] = __builtin_inf();
     for (int i = threadIdx.x; i < npair; i += 256) {
-        const double J = approx_J(a, q, k0 + i / nm, i % nm);
-        lmin = J < lmin ? J : lmin;
+        const int k = k0 + i / nm, m = i % nm;
+        const double sn = a.S[((long long)q.c * a.K + k) * a.M + m] * q.ninv;
+        const double lm = (double)a.lam[m];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            if (r >= q.ne) break;
+            const double J = lm * q.ev[r] + sn;
+            lmin[r] = J < lmin[r] ? J : lmin[r];
+        }
     }
-    const double r = block_min(lmin);
-    if (threadIdx.x == 0) chunk_min[(long long)ec * nchunks + blockIdx.y] = r;
+    block_min_rows<R>(lmin, q.ne);
+    if (threadIdx.x < q.ne) {
+        const int ec = (q.e0 + threadIdx.x) * a.C + q.c;
+        double r = lmin[0];
+#pragma unroll
+        for (int i = 1; i < R; ++i)
+            if (i == (int)threadIdx.x) r = lmin[i];
+        chunk_min[(long long)ec * nchunks + blockIdx.y] = r;
+    }
 }
 
+template <int R>
 __global__ __launch_bounds__(256) void band_collect_kernel(BandArgs a, const double *chunk_min,
                                                            int nchunks)
 {
-    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
-    const BandProblem q = band_problem(a, ec);
-    double lmin = __builtin_inf();
-    for (int i = threadIdx.x; i < nchunks; i += 256) {
-        const double v = chunk_min[(long long)ec * nchunks + i];
-        lmin = v < lmin ? v : lmin;
+    const BandGroup<R> q = band_group<R>(a);
+    double T[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        T[r] = __builtin_inf();
+        if (r < q.ne) {
+            const int ec = (q.e0 + r) * a.C + q.c;
+            for (int i = threadIdx.x; i < nchunks; i += 256) {
+                const double v = chunk_min[(long long)ec * nchunks + i];
+                T[r] = v < T[r] ? v : T[r];
+            }
+        }
     }
-    const double wmin = block_min(lmin);
-    const double T = wmin + kBandTau * wmin + q.slack;
+    block_min_rows<R>(T, q.ne);
+#pragma unroll
+    for (int r = 0; r < R; ++r) T[r] = T[r] + kBandTau * T[r] + q.slack;
     const int k0 = blockIdx.y * kBandKC;
     const int k1 = min(k0 + kBandKC - 1, q.kmax);
     const int nm = q.mlim + 1;
     const int npair = k1 >= k0 ? (k1 - k0 + 1) * nm : 0;
     for (int i = threadIdx.x; i < npair; i += 256) {
         const int k = k0 + i / nm, m = i % nm;
-        if (approx_J(a, q, k, m) <= T) {
-            const int slot = atomicAdd(&a.count[ec], 1);
-            if (slot < kBandCap) a.cand[(long long)ec * kBandCap + slot] = k * a.M + m;
+        const double sn = a.S[((long long)q.c * a.K + k) * a.M + m] * q.ninv;
+        const double lm = (double)a.lam[m];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            if (r >= q.ne) break;
+            if (lm * q.ev[r] + sn <= T[r]) {
+                const int ec = (q.e0 + r) * a.C + q.c;
+                const int slot = atomicAdd(&a.count[ec], 1);
+                if (slot < kBandCap) a.cand[(long long)ec * kBandCap + slot] = k * a.M + m;
+            }
         }
     }
-    if (blockIdx.y == 0 && threadIdx.x == 0) a.thresh[ec] = T;
+    if (blockIdx.y == 0 && threadIdx.x < q.ne) {
+        double t = T[0];
+#pragma unroll
+        for (int i = 1; i < R; ++i)
+            if (i == (int)threadIdx.x) t = T[i];
+        a.thresh[(q.e0 + threadIdx.x) * a.C + q.c] = t;
+    }
 }
 
 hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st)
@@ -225,9 +285,19 @@ hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st)
     int32_t *count = a.count + (a.c_only >= 0 ? (a.e_row * a.C + a.c_only) : 0);
     hipLaunchKernelGGL(fill_u32_kernel, dim3((EC + 255) / 256), dim3(256), 0, st,
                        reinterpret_cast<uint32_t *>(count), (long long)EC, 0u);
-    hipLaunchKernelGGL(band_min_kernel, dim3(EC, nchunks), dim3(256), 0, st, a, chunk_min, nchunks);
-    hipLaunchKernelGGL(band_collect_kernel, dim3(EC, nchunks), dim3(256), 0, st, a,
-                       (const double *)chunk_min, nchunks);
+    if (a.c_only >= 0 || a.E == 1) {
+        const int groups = a.c_only >= 0 ? 1 : a.C;
+        hipLaunchKernelGGL(band_min_kernel<1>, dim3(groups, nchunks), dim3(256), 0, st, a,
+                           chunk_min, nchunks);
+        hipLaunchKernelGGL(band_collect_kernel<1>, dim3(groups, nchunks), dim3(256), 0, st, a,
+                           (const double *)chunk_min, nchunks);
+    } else {
+        const int groups = a.C * ((a.E + kBandE - 1) / kBandE);
+        hipLaunchKernelGGL(band_min_kernel<kBandE>, dim3(groups, nchunks), dim3(256), 0, st, a,
+                           chunk_min, nchunks);
+        hipLaunchKernelGGL(band_collect_kernel<kBandE>, dim3(groups, nchunks), dim3(256), 0, st, a,
+                           (const double *)chunk_min, nchunks);
+    }
     return hipGetLastError();
 }
 
