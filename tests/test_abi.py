@@ -71,3 +71,34 @@ def test_product_has_no_cpu_fallback():
         if fn.endswith(".py"):
             txt = open(os.path.join(pkg, fn)).read()
             assert "import oracle" not in txt and "from oracle" not in txt, fn
+
+
+def test_header_is_plain_c_and_links(lib, tmp_path):
+    """include/dro.h compiles as C99 (no C++ types in the ABI) and a C program
+    that calls through it links against libdro.so (no entry point that needs a
+    device is called: it is only linked)."""
+    import shutil
+    import subprocess
+    from paper_2607_16892_amd import _native
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use_dro.c"
+    src.write_text(
+        '#include "dro.h"\n'
+        "#include <stdio.h>\n"
+        "int main(void) {\n"
+        "    dro_problem p = {0};\n"
+        "    int32_t k = 0; double w = 0.0;\n"
+        "    int rc = dro_argmin_reservation(NULL, &p, 1, NULL, NULL, NULL, &k, &w, NULL, NULL);\n"
+        '    printf("%d %s\\n", rc, dro_strerror(rc));\n'
+        "    return rc == DRO_EINVAL ? 0 : 1;\n"
+        "}\n")
+    exe = tmp_path / "use_dro"
+    libdir = os.path.dirname(_native.LIB_PATH)
+    r = subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-pedantic", "-I",
+                        os.path.join(ROOT, "include"), str(src), "-o", str(exe), "-L", libdir,
+                        "-ldro", f"-Wl,-rpath,{libdir}"], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert run.returncode == 0 and run.stdout.startswith("-1 invalid argument"), run.stdout + run.stderr
