@@ -842,11 +842,15 @@ hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *s
     return hipGetLastError();
 }
 
-// Block per (c, k), thread per multiplier (m = t, t + 256, ...): exact S,
-// exact J for every radius row, and the minimum over m with the lowest m
-// (W, m_star), radius rows in groups of 8 reduced across the block.
+// Block per (class, KB = 256 / TM consecutive grid points), TM threads per
+// grid point (TM = the power of two >= min(M, 256)), each taking the
+// multipliers m = ml, ml + TM, ...: exact S, exact J for every radius row, and
+// per grid point the minimum over m with the lowest m (W, m_star), radius rows
+// in groups of 8 reduced over each grid point's TM threads in LDS.  The lowest
+// (J, m) does not depend on the order of the reduction.
 constexpr int kTableThreads = 256;
 
+template <int TM>
 __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
     const float *lam, const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt,
@@ -855,8 +859,11 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
 {
     __shared__ double rv[8][kTableThreads];
     __shared__ int rm[8][kTableThreads];
-    const long long ck = blockIdx.x;
-    const int c = (int)(ck / K), k = (int)(ck % K), t = threadIdx.x;
+    const int KB = kTableThreads / TM;
+    const int kgroups = (K + KB - 1) / KB;
+    const int c = (int)(blockIdx.x / kgroups);
+    const int t = threadIdx.x, ml = t % TM;
+    const int k = (int)(blockIdx.x % kgroups) * KB + t / TM;
     if (gate && *gate == 0u) return;
     if (need) {  // only the classes some radius row of which needs the table
         bool any = false;
@@ -865,7 +872,7 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     }
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
-    const int64_t L = L_[c], eta = eta_[k];
+    const int64_t L = L_[c], eta = eta_[k < K ? k : K - 1];
     const uint32_t *cn = cnt + (long long)s * kHistBins;
     const uint64_t *sm = sum + (long long)s * kHistBins;
     const int64_t CP = fix33(c_p[c]), CW = fix33(c_w[c]);
@@ -880,7 +887,7 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
             bm[q] = 0x7fffffff;
             ev[q] = (e0 + q < E) ? (double)eps[(long long)(e0 + q) * C + c] : 0.0;
         }
-        for (int m = t; m < M; m += kTableThreads) {
+        for (int m = ml; m < M; m += TM) {
             const unsigned __int128 u = exact_S_prefix(cn, sm, N, L, eta, CP, CW, fix33(lam[m]));
             const double q_ = __ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), Nd);
             const double lm = (double)lam[m];
@@ -902,8 +909,9 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
             rm[q][t] = bm[q];
         }
         __syncthreads();
-        for (int w = kTableThreads / 2; w > 0; w >>= 1) {
-            if (t < w) {
+#pragma unroll
+        for (int w = TM / 2; w > 0; w >>= 1) {  // within each grid point's TM threads
+            if (ml < w) {
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     if (q >= nq) break;
@@ -917,10 +925,13 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
             }
             __syncthreads();
         }
-        if (t < 8 && e0 + t < E) {
-            const long long o = ((long long)(e0 + t) * C + c) * K + k;
-            W[o] = rv[t][0];
-            m_star[o] = rm[t][0];
+        if (k < K) {  // the grid point's threads write its rows, thread ml rows ml, ml + TM, ...
+            const int g0 = t - ml;
+            for (int q = ml; q < nq; q += TM) {
+                const long long o = ((long long)(e0 + q) * C + c) * K + k;
+                W[o] = rv[q][g0];
+                m_star[o] = rm[q][g0];
+            }
         }
         __syncthreads();
     }
@@ -981,10 +992,28 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
                               const int32_t *need, const uint32_t *gate, bool with_prefix)
 {
     if (with_prefix) HIPRET(launch_prefix(hist, S, cnt, sum, st, gate));
-    const long long n = (long long)C * K;
-    hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)n), dim3(kTableThreads), 0, st, offsets,
-                       seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,
-                       (const uint64_t *)sum, E, C, K, M, W, m_star, need, gate);
+    int TM = 1;  // threads per grid point
+    while (TM < M && TM < kTableThreads) TM *= 2;
+    const int KB = kTableThreads / TM;
+    const long long n = (long long)C * ((K + KB - 1) / KB);
+#define DRO_TABLE_CASE(tm)                                                                        \
+    case tm:                                                                                      \
+        hipLaunchKernelGGL(exact_table_kernel<tm>, dim3((unsigned)n), dim3(kTableThreads), 0, st, \
+                           offsets, seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,       \
+                           (const uint64_t *)sum, E, C, K, M, W, m_star, need, gate);            \
+        break;
+    switch (TM) {
+        DRO_TABLE_CASE(1)
+        DRO_TABLE_CASE(2)
+        DRO_TABLE_CASE(4)
+        DRO_TABLE_CASE(8)
+        DRO_TABLE_CASE(16)
+        DRO_TABLE_CASE(32)
+        DRO_TABLE_CASE(64)
+        DRO_TABLE_CASE(128)
+        DRO_TABLE_CASE(256)
+    }
+#undef DRO_TABLE_CASE
     if (k_star)
         hipLaunchKernelGGL(table_argmin_kernel, dim3(E * C), dim3(256), 0, st, (const double *)W,
                            (const int32_t *)m_star, k_max, C, K, k_star, W_star, m_at_star, need,

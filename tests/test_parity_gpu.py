@@ -88,6 +88,7 @@ RANDOM_CASES = [
          cost_choices=[(4.0, 1.0), (8.0, 1.0), (2.0, 2.0)]),               # q N integer: ties
     dict(seed=10, C=6, N=(700, 33, 1500), alias=True, L=2000, K=97, M=40, E=19),  # 19 radii
     dict(seed=11, C=4, N=(256, 511, 512, 16385), L=3000, K=33, M=40, E=2),  # slice-floor sizes
+    dict(seed=12, C=3, N=(300, 41, 2000), L=1500, K=77, M=3, E=8),         # 8 radii, 3 multipliers
 ]
 
 
