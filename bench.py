@@ -41,7 +41,7 @@ VALU_ISSUE_PEAK = 256 * 128 * 2.4e9   # lane-instructions/s of double-rate fp32 
 # stripped, identified by the hash prefix) and are
 # reported as null for any other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "cabffb7d42a45ffc",
+    "dense_code_sha256_16": "82911c48cda0bfd3",
     "workload": "mixture-16x1M",
     "valu_instr_per_eval": 2.0597,       # SQ_INSTS_VALU x 64 / evaluations
     "hbm_bytes_per_launch": 1638297.24 * 1024,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
@@ -50,9 +50,10 @@ DENSE_COUNTERS = {
 
 
 def dense_code_hash() -> str:
-    """Hash of the dense kernel's code and of its launch plan (the plan_dense
-    function of csrc/api.hip, which sets the number of sample slices and so
-    the partial-sum traffic), comments and whitespace removed."""
+    """Hash of the dense kernel's code, of its constants (the dense section of
+    csrc/dro_internal.h) and of its launch plan (the plan_dense function of
+    csrc/api.hip, which sets the number of sample slices and so the
+    partial-sum traffic), comments and whitespace removed."""
     import hashlib
     import re
     def code(name):
@@ -60,7 +61,9 @@ def dense_code_hash() -> str:
             text = re.sub(r"/\*.*?\*/", " ", f.read(), flags=re.S)
         return re.sub(r"//[^\n]*", " ", text)
 
-    consts = [ln for ln in code("dro_internal.h").splitlines() if "constexpr" in ln]
+    hdr = code("dro_internal.h")
+    i = hdr.index("struct DensePlan")  # the dense section's constants come before its structs
+    consts = [ln for ln in hdr[:i].splitlines() if "constexpr" in ln]
     api = code("api.hip")
     i = api.index("constexpr long long kMinWaves")
     plan = api[i:api.index("return pl;", i)]

@@ -300,7 +300,7 @@ size_t refine_bytes(const dro_problem *p, int EC, int num_cu, bool with_hist)
     const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
     return rup((size_t)EC * kBandCap * 4) + rup((size_t)EC * 4) + rup((size_t)EC * 8) +
            rup((size_t)EC * band_chunks(p->K) * 8) + rup((size_t)EC * 4) + rup(4) +
-           (with_hist ? quantile_bytes(p, num_cu) : 0) + rup(bins * 4) + rup(bins * 8) +
+           (with_hist ? quantile_bytes(p, num_cu) : 0) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8) +
            rup(eck * 8) + rup(eck * 4);
 }
 
@@ -316,7 +316,7 @@ RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int num_cu, bool
     r.any = ar.take<uint32_t>(1);
     r.qb = with_hist ? take_quantile(ar, p, num_cu) : QuantBufs{nullptr, nullptr, 0};
     r.cnt = ar.take<uint32_t>(bins);
-    r.sum = ar.take<uint64_t>(bins);
+    r.sum = ar.take<uint64_t>(prefix_sum_words(p->S));
     r.Wt = ar.take<double>(eck);
     r.mt = ar.take<int32_t>(eck);
     return r;
@@ -644,7 +644,7 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -653,7 +653,7 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     p = &q;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
-    uint64_t *sum = ar.take<uint64_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
     HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
     HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, k_max,
                               qb.hist, p->S, E, p->C, p->K, p->M, cnt, sum, W, m_star, k_star,
@@ -672,7 +672,7 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -681,7 +681,7 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     p = &q;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
-    uint64_t *sum = ar.take<uint64_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
     HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
     HIPCHK(launch_continuous_dual(p->offsets, p->seg, p->L, p->eta, p->c_p, p->c_w, eps, qb.hist,
                                   p->S, E, p->C, p->K, cnt, sum, W, gamma, st));
@@ -724,7 +724,7 @@ int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const in
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(bins * 8), st);
+    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -733,7 +733,7 @@ int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const in
     p = &q;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
-    uint64_t *sum = ar.take<uint64_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
     HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
     HIPCHK(launch_reservation_cost(p->offsets, p->seg, p->c_p, p->c_w, qb.hist, p->S, p->C, R,
                                    eta_r, cnt, sum, cost, cover, st));
@@ -1096,7 +1096,7 @@ int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dr
     if (nz > kMaxConfigs) return fail(ctx, DRO_ELIMIT, "%lld configurations exceed 2^32", nz);
     const size_t bins = (size_t)p->S * kHistBins;
     const size_t need = stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) +
-                        rup(bins * 8) + rup((size_t)C * K * 8) + rup((size_t)C * K * 4) +
+                        rup(prefix_sum_words(p->S) * 8) + rup((size_t)C * K * 8) + rup((size_t)C * K * 4) +
                         4 * rup((size_t)C * 8) + rup(lp1_tableau_doubles(C, G) * 8) +
                         rup((size_t)m * 4) + 4 * rup((size_t)CG * 8) + 2 * rup((size_t)CG) +
                         7 * rup((size_t)G * 8) + 6 * rup((size_t)C * 8) +
@@ -1111,7 +1111,7 @@ int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dr
     const SvcArgs s = svc_args(svc, C);
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *pcnt = ar.take<uint32_t>(bins);
-    uint64_t *psum = ar.take<uint64_t>(bins);
+    uint64_t *psum = ar.take<uint64_t>(prefix_sum_words(p->S));
     double *W = ar.take<double>((size_t)C * K);
     int32_t *mstar = ar.take<int32_t>((size_t)C * K);
     int64_t *cnt = ar.take<int64_t>(C), *sum = ar.take<int64_t>(C), *ssq = ar.take<int64_t>(C);

@@ -121,11 +121,20 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
                          int64_t *q_rank, hipStream_t st);
 
 // ---- exact table (value counts and prefix sums) -------------------------------
+// The prefix pass works in chunks of 4096 bins.  A sum array holds the S x
+// kHistBins prefix sums followed by S x kPrefixChunks (count, sum) chunk totals
+// that the pass uses as scratch: prefix_sum_words(S) u64 in all.
+constexpr int kPrefixChunk = 4096;
+constexpr int kPrefixChunks = (kHistBins + kPrefixChunk - 1) / kPrefixChunk;
+inline size_t prefix_sum_words(int S)
+{
+    return (size_t)S * kHistBins + (size_t)S * kPrefixChunks * 2;
+}
 // cnt[s][v] = #{x <= v}, sum[s][v] = sum of the samples <= v of segment s, from
 // its value histogram; with a gate, nothing runs while *gate is 0.
 hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
                          const uint32_t *gate = nullptr);
-// cnt: [S][kHistBins] u32, sum: [S][kHistBins] u64 scratch; k_star == null skips the argmin.
+// cnt: [S][kHistBins] u32, sum: prefix_sum_words(S) u64 scratch; k_star == null skips the argmin.
 // With need ([E*C]), only the rows with need[e*C + c] != 0 are computed and only
 // their k_star, W_star, m_at_star written; with a gate, nothing runs while *gate is 0.
 // with_prefix = false takes cnt and sum as already formed from hist.

@@ -758,34 +758,34 @@ namespace dro {
 // evaluated in 128-bit integers in units of 2^-33: exact.
 
 // Per segment: cnt[v] = #{x <= v} (u32) and sum[v] = sum of the samples <= v
-// (u64), from the value histogram.  Block (segment, chunk) handles 4096 bins:
-// it sums the bins before its chunk (coalesced), stages the chunk in LDS
-// (padded to spread the per-thread runs over the banks), scans it (16
-// consecutive bins per thread, then across threads) and stores each thread's
-// run of prefixes.
-constexpr int kPrefixChunk = 4096;
+// (u64), from the value histogram, in two passes over blocks of (segment,
+// chunk of 4096 bins): the chunk totals, then per chunk the sum of the totals
+// before it, the chunk staged in LDS (padded to spread the per-thread runs over
+// the banks) and scanned (16 consecutive bins per thread, then across threads),
+// and each thread's run of prefixes stored.
 constexpr int kPrefixThreads = 256;
 constexpr int kPrefixPer = kPrefixChunk / kPrefixThreads;  // 16
 
 __device__ __forceinline__ int pad32(int j) { return j + (j >> 5); }
 
-__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *hist, uint32_t *cnt,
-                                                                uint64_t *sum, const uint32_t *gate)
+// Per (segment, chunk): the count and the value-weighted sum of the chunk's
+// bins, tot[(s * kPrefixChunks + ch) * 2 + {0, 1}].
+__global__ __launch_bounds__(kPrefixThreads) void chunk_total_kernel(const uint32_t *hist,
+                                                                     uint64_t *tot,
+                                                                     const uint32_t *gate)
 {
-    __shared__ uint32_t hc[kPrefixChunk + kPrefixChunk / 32];
     __shared__ uint64_t rc[kPrefixThreads], rs[kPrefixThreads];
     if (gate && *gate == 0u) return;
-    constexpr int kChunks = (kHistBins + kPrefixChunk - 1) / kPrefixChunk;
-    const int ch = (int)(blockIdx.x % kChunks), s = (int)(blockIdx.x / kChunks), t = threadIdx.x;
+    const int ch = (int)(blockIdx.x % kPrefixChunks), s = (int)(blockIdx.x / kPrefixChunks);
+    const int t = threadIdx.x;
     const uint32_t *h = hist + (long long)s * kHistBins;
-    const int v0 = ch * kPrefixChunk, v1 = min(kHistBins, v0 + kPrefixChunk), n = v1 - v0;
-    uint64_t bc = 0, bs = 0;  // everything before the chunk
-    for (int v = t; v < v0; v += kPrefixThreads) {
+    const int v0 = ch * kPrefixChunk, v1 = min(kHistBins, v0 + kPrefixChunk);
+    uint64_t bc = 0, bs = 0;
+    for (int v = v0 + t; v < v1; v += kPrefixThreads) {
         const uint64_t x = h[v];
         bc += x;
         bs += x * (uint64_t)v;
     }
-    for (int j = t; j < n; j += kPrefixThreads) hc[pad32(j)] = h[v0 + j];
     rc[t] = bc;
     rs[t] = bs;
     __syncthreads();
@@ -796,7 +796,30 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *
         }
         __syncthreads();
     }
-    const uint64_t base_c = rc[0], base_s = rs[0];
+    if (t == 0) {
+        tot[(long long)blockIdx.x * 2] = rc[0];
+        tot[(long long)blockIdx.x * 2 + 1] = rs[0];
+    }
+}
+
+__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *hist,
+                                                                const uint64_t *tot, uint32_t *cnt,
+                                                                uint64_t *sum, const uint32_t *gate)
+{
+    __shared__ uint32_t hc[kPrefixChunk + kPrefixChunk / 32];
+    __shared__ uint64_t rc[kPrefixThreads / 64], rs[kPrefixThreads / 64];
+    if (gate && *gate == 0u) return;
+    const int ch = (int)(blockIdx.x % kPrefixChunks), s = (int)(blockIdx.x / kPrefixChunks);
+    const int t = threadIdx.x;
+    const uint32_t *h = hist + (long long)s * kHistBins;
+    const int v0 = ch * kPrefixChunk, v1 = min(kHistBins, v0 + kPrefixChunk), n = v1 - v0;
+    for (int j = t; j < n; j += kPrefixThreads) hc[pad32(j)] = h[v0 + j];
+    uint64_t base_c = 0, base_s = 0;  // everything before the chunk, in chunk order
+    const uint64_t *tt = tot + (long long)s * kPrefixChunks * 2;
+    for (int i = 0; i < ch; ++i) {
+        base_c += tt[2 * i];
+        base_s += tt[2 * i + 1];
+    }
     __syncthreads();
     const int a = t * kPrefixPer;
     uint64_t lc = 0, ls = 0;
@@ -808,17 +831,27 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *
             ls += x * (uint64_t)(v0 + j);
         }
     }
-    rc[t] = lc;
-    rs[t] = ls;
-    __syncthreads();
-    for (int w = 1; w < kPrefixThreads; w <<= 1) {  // inclusive scans
-        const uint64_t ac = t >= w ? rc[t - w] : 0, as = t >= w ? rs[t - w] : 0;
-        __syncthreads();
-        rc[t] += ac;
-        rs[t] += as;
-        __syncthreads();
+    // inclusive scans of the thread totals: shuffles within each wave, then
+    // the totals of the waves before
+    const int lane = t & 63, wave = t >> 6;
+    uint64_t ic = lc, is = ls;
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t oc = __shfl_up(ic, d, 64), os = __shfl_up(is, d, 64);
+        if (lane >= d) {
+            ic += oc;
+            is += os;
+        }
     }
-    uint64_t c = base_c + rc[t] - lc, x = base_s + rs[t] - ls;
+    if (lane == 63) {
+        rc[wave] = ic;
+        rs[wave] = is;
+    }
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) {
+        ic += rc[w];
+        is += rs[w];
+    }
+    uint64_t c = base_c + ic - lc, x = base_s + is - ls;
     uint32_t *gc = cnt + (long long)s * kHistBins + v0;
     uint64_t *gs = sum + (long long)s * kHistBins + v0;
     for (int i = 0; i < kPrefixPer; ++i) {
@@ -836,9 +869,14 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *
 hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
                          const uint32_t *gate)
 {
-    const long long blocks = (long long)S * ((kHistBins + kPrefixChunk - 1) / kPrefixChunk);
+    // chunk totals first (after the prefix sums in the same array), then each
+    // chunk's scan starts from the totals of the chunks before it
+    const long long blocks = (long long)S * kPrefixChunks;
+    uint64_t *tot = sum + (long long)S * kHistBins;
+    hipLaunchKernelGGL(chunk_total_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st,
+                       hist, tot, gate);
     hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st, hist,
-                       cnt, sum, gate);
+                       (const uint64_t *)tot, cnt, sum, gate);
     return hipGetLastError();
 }
 
