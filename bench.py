@@ -321,20 +321,24 @@ def main():
     m_star = torch.empty((E, w.C, w.K), dtype=torch.int32, device=dev)
     outs = {}
 
-    def step(ev_pair=None):
+    def step(ev=None):
+        if ev:
+            ev[0].record()
         dro.class_quantile(ctx, prob)
-        if ev_pair:
-            ev_pair[0].record()
+        if ev:
+            ev[1].record()
         dro.dro_cost_eval(ctx, prob, eps, W=W, m_star=m_star, S=S)
-        if ev_pair:
-            ev_pair[1].record()
+        if ev:
+            ev[2].record()
         outs.update(dro.dro_argmin_reservation(ctx, prob, eps, S))
+        if ev:
+            ev[3].record()
 
     _log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    pairs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
              for _ in range(args.steps)]
     _log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
@@ -345,8 +349,13 @@ def main():
     t1 = time.perf_counter()
     flags = ctx.take_flags()
     ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
-    launch_times = [a.elapsed_time(b) for a, b in pairs]
+    launch_times = [e[1].elapsed_time(e[2]) for e in pairs]
     dense_ms = float(np.mean(launch_times))
+    breakdown = {"quantile_ms": float(np.median([e[0].elapsed_time(e[1]) for e in pairs])),
+                 "cost_eval_ms": float(np.median(launch_times)),
+                 "argmin_ms": float(np.median([e[2].elapsed_time(e[3]) for e in pairs])),
+                 "note": "HIP events on the launch stream around class_quantile, dro_cost_eval "
+                         "and dro_argmin_reservation; medians over the timed steps"}
     evals = w.evals
     value = evals / (ms_step / 1e3)
     achieved = evals * FLOPS_PER_EVAL / (dense_ms / 1e3) / 1e12
@@ -449,6 +458,7 @@ def main():
                      "valu_issue_frac": (evals * cnt["valu_instr_per_eval"] / (dense_ms / 1e3)
                                          / VALU_ISSUE_PEAK) if cnt else None,
                      "counters": cnt["source"] if cnt else None},
+        "step_breakdown": breakdown,
         "cpu_baseline": cpu,
         "block_step": bcd,
         "policy_comparison": pol,
