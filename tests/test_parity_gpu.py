@@ -89,6 +89,7 @@ RANDOM_CASES = [
     dict(seed=10, C=6, N=(700, 33, 1500), alias=True, L=2000, K=97, M=40, E=19),  # 19 radii
     dict(seed=11, C=4, N=(256, 511, 512, 16385), L=3000, K=33, M=40, E=2),  # slice-floor sizes
     dict(seed=12, C=3, N=(300, 41, 2000), L=1500, K=77, M=3, E=8),         # 8 radii, 3 multipliers
+    dict(seed=13, C=2, N=(500, 60), L=700, K=50, M=2, E=3),                 # 2 multipliers
 ]
 
 
