@@ -38,7 +38,9 @@
  *    read outside the segments given by the offsets, whatever the data.
  *  - A ctx is not thread-safe: use one ctx per host thread / stream.
  *  - Exactness limits (DRO_ELIMIT when exceeded): 0 <= x, eta <= L <= 2^15,
- *    N_c <= 2^26 samples per class, every lam, c_p, c_w in [2^-10, 2^7].
+ *    N_c <= 2^26 samples per class, every lam, c_p, c_w in [2^-10, 2^7];
+ *    K <= 2^15 + 1 grid points, M <= 65536 multipliers, K * M < 2^31 pairs
+ *    and E * C < 2^31 radius rows.
  *    Inside them every candidate of phi is a multiple of 2^-33 below 2^56, so
  *    the library can evaluate S exactly in 128-bit fixed point where the
  *    result is an index (argmin, quantile) or the reported optimum.

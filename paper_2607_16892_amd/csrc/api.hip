@@ -125,6 +125,8 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
         return fail(ctx, DRO_EINVAL, "without a segment map S must equal C (S=%d C=%d)", p->S, p->C);
     if (p->K > 32769) return fail(ctx, DRO_ELIMIT, "K=%d exceeds 2^15 + 1 grid points", p->K);
     if (p->M > 65536) return fail(ctx, DRO_ELIMIT, "M=%d exceeds 65536 multipliers", p->M);
+    if ((long long)p->K * p->M > 0x7fffffffLL)  // the exact argmin packs (k, m) as k M + m in 31 bits
+        return fail(ctx, DRO_ELIMIT, "K*M = %lld exceeds 2^31 - 1 grid pairs", (long long)p->K * p->M);
     const int64_t *o = p->offsets_h;
     if (o[0] != 0) return fail(ctx, DRO_EINVAL, "offsets[0] must be 0");
     for (int s = 0; s < p->S; ++s)
@@ -405,6 +407,14 @@ int run_quantile(dro_ctx *ctx, const dro_problem *p, const QuantBufs &qb, int32_
     return DRO_OK;
 }
 
+// E radius rows of C classes are indexed as e C + c in 32 bits.
+int check_rows(dro_ctx *ctx, int E, int C)
+{
+    if ((long long)E * C > 0x7fffffffLL)
+        return fail(ctx, DRO_ELIMIT, "E*C = %lld radius rows exceed 2^31 - 1", (long long)E * C);
+    return DRO_OK;
+}
+
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 bool in_limits(float v) { return v >= 0x1p-10f && v <= 0x1p7f; }
 
@@ -567,6 +577,7 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     int rc = check_problem(ctx, p, &sh);
     if (rc) return rc;
     if (E <= 0 || !eps || !W) return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W non-NULL");
+    if ((rc = check_rows(ctx, E, p->C))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
@@ -596,6 +607,7 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     if (rc) return rc;
     if (E <= 0 || !eps || !S || !k_star || !W_star)
         return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, S, k_star, W_star non-NULL");
+    if ((rc = check_rows(ctx, E, p->C))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int EC = E * p->C;
@@ -641,6 +653,7 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     if (rc) return rc;
     if (E <= 0 || !eps || !W || !m_star || (k_star && !W_star))
         return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, m_star (and W_star with k_star) non-NULL");
+    if ((rc = check_rows(ctx, E, p->C))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
@@ -669,6 +682,7 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     if (rc) return rc;
     if (E <= 0 || !eps || !W || !gamma)
         return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, gamma non-NULL");
+    if ((rc = check_rows(ctx, E, p->C))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;

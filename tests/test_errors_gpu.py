@@ -128,6 +128,12 @@ def test_host_checks_and_untouched_outputs(ctx, dev):
     bad = prob.struct()
     bad.K = 40000
     assert call(bad) == ELIMIT
+    # K and M each at their limit, but K * M beyond 2^31 - 1 grid pairs
+    bad = prob.struct()
+    bad.K = 32769
+    bad.M = 65536
+    assert call(bad) == ELIMIT
+    assert "K*M" in ctx.last_error()
     # a class beyond 2^26 samples (rejected from the host offsets alone)
     big = w.offsets.copy()
     big[1:] += (1 << 26) + 1 - int(w.offsets[1])
