@@ -226,6 +226,27 @@ int class_moments(dro_ctx *ctx, const dro_problem *p, int64_t *count, int64_t *s
 int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const int32_t *eta_r,
                          double *cost, int64_t *cover, dro_stream_t stream);
 
+/* The moment-based and block-aligned baseline reservations that the policy
+ * comparison prices against DRO (Sec. 5.1: the mean and P95 with block
+ * alignment; Sec. 5.4: mean plus k standard deviations), exactly in integers,
+ * from the per-class count n, sum s and sum of squares ss of class_moments:
+ *   mean_r[c]       = ceil(s / n), the least integer >= the mean
+ *   lp_r[i*C + c]   = min(L[c], the least integer >= mean + k_i sigma), sigma
+ *                     the population standard deviation; equivalently
+ *                     ceil((s + ceil(sqrt(k_i^2 (n ss - s^2)))) / n)
+ *   block_r[c]      = q[c] rounded up to a multiple of `block` tokens
+ * for i = 0..nk-1 with k_i = k_sigma_h[i] (HOST array, integers in [0, 64],
+ * nk <= 8).  count, sum, sumsq (int64), L, q (int32) and the outputs (int32)
+ * are device arrays of length C (lp_r: nk*C); q and block_r are NULL together
+ * (block >= 1 when given), lp_r and k_sigma_h may be NULL when nk = 0.
+ * Violations give DRO_EINVAL before any work is enqueued.  The square root is
+ * a double estimate corrected with exact 128-bit products. */
+int dro_baseline_reservations(dro_ctx *ctx, int32_t C, const int64_t *count, const int64_t *sum,
+                              const int64_t *sumsq, const int32_t *L, int32_t nk,
+                              const int32_t *k_sigma_h, const int32_t *q, int32_t block,
+                              int32_t *mean_r, int32_t *lp_r, int32_t *block_r,
+                              dro_stream_t stream);
+
 /* Initial state of Alg. 1: r0 = L_in + E[xi], i.e. k0[c] = the largest k with
  * eta[k] <= mean of the class samples (compared exactly). */
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream);

@@ -6,12 +6,14 @@ names.  Import fails loudly at first use if the library is not built.
 """
 from .api import (Context, Problem, Groups, DroError, dro_validate, dro_cost_eval,
                   dro_argmin_reservation, dro_exact_table, dro_continuous_dual, class_quantile,
-                  class_moments, dro_reservation_cost, bcd_init_state, bcd_block_step,
+                  class_moments, dro_reservation_cost, dro_baseline_reservations, bcd_init_state,
+                  bcd_block_step,
                   DRO_FLAG_BAND_FULL, DRO_FLAG_BAND_MARGIN)
 from ._native import LIB_PATH, NativeMissing, load as load_native
 
 __all__ = ["Context", "Problem", "Groups", "DroError", "dro_validate", "dro_cost_eval",
            "dro_argmin_reservation", "dro_exact_table", "dro_continuous_dual", "class_quantile",
-           "class_moments", "dro_reservation_cost", "bcd_init_state", "bcd_block_step",
+           "class_moments", "dro_reservation_cost", "dro_baseline_reservations", "bcd_init_state",
+           "bcd_block_step",
            "DRO_FLAG_BAND_FULL", "DRO_FLAG_BAND_MARGIN", "LIB_PATH", "NativeMissing",
            "load_native"]

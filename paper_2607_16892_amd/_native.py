@@ -51,6 +51,7 @@ EXPORTS = {
     "dro_continuous_dual": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P]),
     "class_moments": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P, P, P, P]),
     "dro_reservation_cost": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P]),
+    "dro_baseline_reservations": (ct.c_int, [P, i32, P, P, P, P, i32, P, P, i32, P, P, P, P]),
     "bcd_init_state": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P]),
     "bcd_service_times": (ct.c_int, [P, ct.POINTER(ProblemStruct), ct.POINTER(ServiceStruct), P, P,
                                      P]),

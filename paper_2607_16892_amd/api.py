@@ -298,6 +298,30 @@ def class_moments(ctx: Context, prob: Problem, stream=None) -> dict:
     return out
 
 
+def dro_baseline_reservations(ctx: Context, moments: dict, L: torch.Tensor, k_sigma=(),
+                              q: Optional[torch.Tensor] = None, block: int = 16,
+                              stream=None) -> dict:
+    """Mean, mean + k sigma and block-aligned reservations from class moments
+    (see dro_baseline_reservations in dro.h)."""
+    dev = L.device
+    C = int(L.shape[0])
+    for name in ("count", "sum", "sumsq"):
+        _need_dev(moments[name], torch.int64, name, dev)
+    _need_dev(L, torch.int32, "L", dev)
+    if q is not None:
+        _need_dev(q, torch.int32, "q", dev)
+    ks = np.ascontiguousarray(list(k_sigma), dtype=np.int32)
+    out = dict(mean=torch.empty(C, dtype=torch.int32, device=dev),
+               lp=torch.empty((len(ks), C), dtype=torch.int32, device=dev),
+               block=None if q is None else torch.empty(C, dtype=torch.int32, device=dev))
+    rc = ctx._lib.dro_baseline_reservations(
+        ctx.handle, C, _ptr(moments["count"]), _ptr(moments["sum"]), _ptr(moments["sumsq"]),
+        _ptr(L), len(ks), ks.ctypes.data if len(ks) else None, _ptr(q), block, _ptr(out["mean"]),
+        _ptr(out["lp"]) if len(ks) else None, _ptr(out["block"]), _stream(stream, dev))
+    ctx.check(rc, "dro_baseline_reservations")
+    return out
+
+
 def dro_reservation_cost(ctx: Context, prob: Problem, eta_r: torch.Tensor, stream=None) -> dict:
     """Average cost of reservations eta_r[R, C] (see dro_reservation_cost in dro.h)."""
     dev = prob.device

@@ -754,6 +754,33 @@ int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const in
     return DRO_OK;
 }
 
+int dro_baseline_reservations(dro_ctx *ctx, int32_t C, const int64_t *count, const int64_t *sum,
+                              const int64_t *sumsq, const int32_t *L, int32_t nk,
+                              const int32_t *k_sigma_h, const int32_t *q, int32_t block,
+                              int32_t *mean_r, int32_t *lp_r, int32_t *block_r,
+                              dro_stream_t stream)
+{
+    if (!ctx) return DRO_EINVAL;
+    if (C <= 0 || !count || !sum || !sumsq || !L || !mean_r)
+        return fail(ctx, DRO_EINVAL, "C must be > 0 and count, sum, sumsq, L, mean_r non-NULL");
+    if (nk < 0 || nk > kMaxBaselineKs || (nk > 0 && (!k_sigma_h || !lp_r)))
+        return fail(ctx, DRO_EINVAL, "nk must be in [0, %d], with k_sigma and lp_r when > 0",
+                    kMaxBaselineKs);
+    if ((q == nullptr) != (block_r == nullptr) || (q && block < 1))
+        return fail(ctx, DRO_EINVAL, "q and block_r go together, with block >= 1");
+    BaselineKs ks{};
+    ks.n = nk;
+    for (int i = 0; i < nk; ++i) {
+        if (k_sigma_h[i] < 0 || k_sigma_h[i] > 64)
+            return fail(ctx, DRO_EINVAL, "k_sigma[%d] = %d outside [0, 64]", i, k_sigma_h[i]);
+        ks.k[i] = k_sigma_h[i];
+    }
+    ENTER_DEVICE(ctx);
+    HIPCHK(launch_baselines(C, count, sum, sumsq, L, ks, q, block, mean_r, lp_r, block_r,
+                            (hipStream_t)stream));
+    return DRO_OK;
+}
+
 int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t stream)
 {
     Shape sh;

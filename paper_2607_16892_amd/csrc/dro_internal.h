@@ -162,6 +162,16 @@ hipError_t launch_reservation_cost(const int64_t *offsets, const int32_t *seg, c
                                    const int32_t *eta_r, uint32_t *cnt, uint64_t *sum,
                                    double *cost, int64_t *cover, hipStream_t st);
 
+// ---- baseline reservations (policy comparison) ---------------------------------
+constexpr int kMaxBaselineKs = 8;
+struct BaselineKs {
+    int n;                    // number of multiples k of the standard deviation
+    int k[kMaxBaselineKs];    // each in [0, 64]
+};
+hipError_t launch_baselines(int C, const int64_t *count, const int64_t *sum, const int64_t *sumsq,
+                            const int32_t *L, const BaselineKs &ks, const int32_t *q, int block,
+                            int32_t *mean_r, int32_t *lp_r, int32_t *block_r, hipStream_t st);
+
 // ---- block step ----------------------------------------------------------------
 // sums: [C] scratch
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,

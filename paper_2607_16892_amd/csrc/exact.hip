@@ -1063,6 +1063,62 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
 
 namespace dro {
 
+// ================================================== baseline reservations ====
+// The moment-based and block-aligned baselines of the policy comparison
+// (Sec. 5.1: the mean and the block-aligned P95; Sec. 5.4: mean + k sigma), one
+// thread per class, exactly in integers:
+//   mean_r        = ceil(s / n)
+//   lp_r[i]       = min(L, the least integer r with r n - s >= k_i sqrt(n ss - s^2)),
+//                   i.e. ceil((s + ceil(sqrt(k_i^2 (n ss - s^2)))) / n)
+//   block_r       = q rounded up to a multiple of `block`
+// with n, s, ss the count, sum and sum of squares of the class samples.
+
+// ceil(sqrt(d)) for d < 2^100: a double estimate corrected with exact products
+__device__ uint64_t ceil_sqrt_u128(unsigned __int128 d)
+{
+    uint64_t r = (uint64_t)sqrt((double)d);
+    while (r > 0 && (unsigned __int128)r * r > d) --r;
+    while ((unsigned __int128)(r + 1) * (r + 1) <= d) ++r;
+    return r + ((unsigned __int128)r * r < d ? 1u : 0u);
+}
+
+__device__ __forceinline__ int64_t ceil_div_pos(__int128 a, int64_t b)
+{
+    return (int64_t)((a + b - 1) / b);  // a >= 0, b >= 1
+}
+
+__global__ void baseline_kernel(int C, const int64_t *count, const int64_t *sum,
+                                const int64_t *sumsq, const int32_t *L, BaselineKs ks,
+                                const int32_t *q, int block, int32_t *mean_r, int32_t *lp_r,
+                                int32_t *block_r)
+{
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    const int64_t n = count[c] > 0 ? count[c] : 1, s = sum[c], ss = sumsq[c];
+    mean_r[c] = (int32_t)ceil_div_pos(s, n);
+    const __int128 v = (__int128)n * ss - (__int128)s * s;  // n^2 times the population variance
+    const unsigned __int128 var = v > 0 ? (unsigned __int128)v : 0;
+    for (int i = 0; i < ks.n; ++i) {
+        const uint64_t k = (uint64_t)ks.k[i];
+        const uint64_t r = ceil_sqrt_u128(var * (k * k));
+        const int64_t lp = ceil_div_pos((__int128)s + r, n);
+        lp_r[(long long)i * C + c] = (int32_t)(lp < L[c] ? lp : L[c]);
+    }
+    if (q && block_r) {
+        const int64_t v0 = q[c] > 0 ? q[c] : 0;
+        block_r[c] = (int32_t)(((v0 + block - 1) / block) * block);
+    }
+}
+
+hipError_t launch_baselines(int C, const int64_t *count, const int64_t *sum, const int64_t *sumsq,
+                            const int32_t *L, const BaselineKs &ks, const int32_t *q, int block,
+                            int32_t *mean_r, int32_t *lp_r, int32_t *block_r, hipStream_t st)
+{
+    hipLaunchKernelGGL(baseline_kernel, dim3((C + 255) / 256), dim3(256), 0, st, C, count, sum,
+                       sumsq, L, ks, q, block, mean_r, lp_r, block_r);
+    return hipGetLastError();
+}
+
 // ====================================================== continuous dual ====
 // W(eta) = min over gamma >= 0 of gamma eps + S(gamma) / N, the Kantorovich
 // dual (Appendix A, Step 3) with gamma continuous (= the LP of Step 5 by

@@ -15,19 +15,18 @@ dro_reservation_cost:
   LP+k sigma the smallest integer >= mean + k * population standard
              deviation (class_moments), at most L, for k = 1, 2
 
-The only host arithmetic is the integer rounding of the moment-based
-baselines: r = ceil((sum + ceil(sqrt(k^2 (N sumsq - sum^2)))) / N).
+Every reservation is computed by the library (the moment-based and
+block-aligned ones by dro_baseline_reservations, exactly in integers); this
+module only selects and stacks them.
 """
 from __future__ import annotations
 
 import dataclasses
-import math
 
-import numpy as np
 import torch
 
-from .api import (Context, Problem, class_moments, class_quantile, dro_exact_table,
-                  dro_reservation_cost)
+from .api import (Context, Problem, class_moments, class_quantile, dro_baseline_reservations,
+                  dro_exact_table, dro_reservation_cost)
 
 BLOCK = 16
 BASELINES = ("SAA", "P90", "P95", "P99", "Mean", "Max", "LP+1sigma", "LP+2sigma")
@@ -44,35 +43,21 @@ def _quantile_at(ctx: Context, prob: Problem, cp: float, cw: float) -> torch.Ten
     return class_quantile(ctx, p)["q_value"]
 
 
-def _ceil_sqrt(d: int) -> int:
-    r = math.isqrt(d)
-    return r + (r * r < d)
-
-
 def reservations(ctx: Context, train: Problem, eps: torch.Tensor) -> torch.Tensor:
     """[R, C] int32 device tensor of every policy's reservation per class."""
-    dev = train.device
-    C = train.C
     ex = dro_exact_table(ctx, train, eps)
     rows = [train.eta[ex["k_star"][e].long()] for e in range(ex["k_star"].shape[0])]
     rows.append(class_quantile(ctx, train)["q_value"])
     rows.append(_quantile_at(ctx, train, 9.0, 1.0))
     p95 = _quantile_at(ctx, train, 19.0, 1.0)
-    rows.append(torch.div(p95 + (BLOCK - 1), BLOCK, rounding_mode="floor") * BLOCK)
+    b = dro_baseline_reservations(ctx, class_moments(ctx, train), train.L, k_sigma=(1, 2), q=p95,
+                                  block=BLOCK)
+    rows.append(b["block"])
     rows.append(_quantile_at(ctx, train, 99.0, 1.0))
-    mo = {k: v.cpu().numpy() for k, v in class_moments(ctx, train).items()}
-    L = train.L.cpu().numpy()
-    mean_r, lp = np.empty(C, np.int64), {1: np.empty(C, np.int64), 2: np.empty(C, np.int64)}
-    for c in range(C):
-        n, s, ss = int(mo["count"][c]), int(mo["sum"][c]), int(mo["sumsq"][c])
-        mean_r[c] = -(-s // n)
-        for k in (1, 2):
-            num = s + _ceil_sqrt(k * k * (n * ss - s * s))
-            lp[k][c] = min(-(-num // n), int(L[c]))
-    rows.append(torch.from_numpy(mean_r).to(dev))
+    rows.append(b["mean"])
     rows.append(train.L)
-    rows.append(torch.from_numpy(lp[1]).to(dev))
-    rows.append(torch.from_numpy(lp[2]).to(dev))
+    rows.append(b["lp"][0])
+    rows.append(b["lp"][1])
     return torch.stack([r.to(torch.int32) for r in rows])
 
 

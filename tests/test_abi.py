@@ -61,6 +61,8 @@ def test_null_context_is_rejected_without_device_work(lib):
                                       None) == -1
     assert lib.class_quantile(None, ct.byref(ps), None, None, None) == -1
     assert lib.bcd_block_step(None, ct.byref(ps), None, None, None, None, None) == -1
+    assert lib.dro_baseline_reservations(None, 1, None, None, None, None, 0, None, None, 16, None,
+                                         None, None, None) == -1
     assert lib.dro_last_error(None) == b"no context"
 
 

@@ -71,3 +71,34 @@ def test_full_table_against_stored_oracle(ctx, dev):
                cost=np.array([[[float.fromhex(v) for v in r] for r in rs] for rs in gold["cost"]]),
                cost_train=np.array([[float.fromhex(v) for v in r] for r in gold["cost_train"]]))
     _same(g, ref)
+
+
+@pytest.mark.parametrize("dist", ["lognormal", "constant"])
+def test_baseline_reservations_against_oracle(ctx, dev, dist):
+    """dro_baseline_reservations (mean, mean + k sigma for k = 0, 1, 2, 3, 8, and
+    a block-aligned quantile) against the oracle's rational definitions, on
+    ragged classes: one sample, all-equal samples, the largest support."""
+    import math
+    from fractions import Fraction
+
+    import torch
+    import oracle.policies as op
+    import paper_2607_16892_amd as dro
+    from workloads import random_workload
+    w = random_workload(seed=78, C=5, N=(1, 40, 2000, 777, 5000), L=32768, K=9, M=4, E=1,
+                        dist=dist)
+    print(f"[gpu] baseline reservations {w.name} dist={dist} N={w.offsets[-1]}", flush=True)
+    prob = dro.Problem.from_workload(w, dev)
+    ks = (0, 1, 2, 3, 8)
+    q = dro.class_quantile(ctx, prob)["q_value"]
+    b = dro.dro_baseline_reservations(ctx, dro.class_moments(ctx, prob), prob.L, k_sigma=ks, q=q,
+                                      block=16)
+    torch.cuda.synchronize()
+    qh = q.cpu().numpy()
+    for c in range(w.C):
+        xs = w.samples_of(c)
+        L = int(w.L[c])
+        assert int(b["mean"][c]) == math.ceil(Fraction(int(xs.astype(np.int64).sum()), len(xs)))
+        for i, k in enumerate(ks):
+            assert int(b["lp"][i, c]) == op._mean_plus(xs, k, L), (c, k)
+        assert int(b["block"][c]) == -(-int(qh[c]) // 16) * 16
