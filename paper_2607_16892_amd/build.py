@@ -26,7 +26,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-result"]
 UNITS = {
-    "dense.hip": [],
+    "dense.hip": ["-ffp-contract=off"],
     "exact.hip": ["-ffp-contract=off"],
     "serving.hip": ["-ffp-contract=off"],
     "api.hip": ["-ffp-contract=off"],

@@ -146,24 +146,22 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
     return DRO_OK;
 }
 
-// Tiles of kTK x kTM pairs per lane; the samples of every class are split into
-// the same P slices (P <= 64, and the largest class's slices hold at least
-// kMinSlice samples; a smaller class's may be short or empty, which adds zero),
-// each handled by its own blocks,
-// whose partial sums of S a reduce kernel adds in a fixed order.  P is the
-// smallest whose grid fills its last wave of resident blocks (CUs x blocks
-// per CU) to at least 97 % and runs at least kMinWaves such waves; failing
-// that, the well-filled P with the most waves, else the best-filled P.  Many
-// short blocks keep the end of the launch from waiting on a few long ones and
-// keep each block's sample slice small; on the 16 x 1e6 workload 32 waves ran
-// 4.6 % faster than 4, and beyond 32 nothing changed.  The partial sums are
-// kept within kPartialBytes.
+// Tiles of kTM pairs per lane; the samples of every class are split into the
+// same P slices (P <= 64, and the largest class's slices hold at least
+// kMinSlice samples; a smaller class's may be short or empty, which adds
+// zero), each handled by its own blocks, which add their exact integer sums
+// into one table.  P is the smallest whose grid fills its last wave of
+// resident blocks (CUs x blocks per CU) to at least 97 % and runs at least
+// kMinWaves such waves; failing that, the well-filled P with the most waves,
+// else the best-filled P.  Many short blocks keep the end of the launch from
+// waiting on a few long ones: compute units do not all run at the same speed,
+// and with a few long waves the ones that finish first idle at the end.
 // The kernels index with the host-validated offsets and segment map: both are
 // copied into the workspace at the start of every call, so device data that
 // disagrees with the host copies can never steer a kernel outside xi.
 constexpr long long kMinWaves = 32;
 constexpr long long kMinSlice = 64;
-constexpr long long kPartialBytes = 2LL << 30;
+constexpr long long kMaxSlices = 64;
 
 size_t stage_bytes(const dro_problem *p)
 {
@@ -191,13 +189,13 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     pl.lanes_m = 1;
     while (pl.lanes_m < need_m && pl.lanes_m < kThreads) pl.lanes_m *= 2;
     pl.lanes_k = kThreads / pl.lanes_m;
-    pl.tiles_k = (K + kTK * pl.lanes_k - 1) / (kTK * pl.lanes_k);
+    pl.tiles_k = (K + pl.lanes_k - 1) / pl.lanes_k;
     pl.tiles_m = (M + kTM * pl.lanes_m - 1) / (kTM * pl.lanes_m);
-    const long long base = (long long)C * pl.tiles_k * pl.tiles_m;
+    pl.tiles = pl.tiles_k * pl.tiles_m;
+    pl.group = std::min(pl.tiles, kTileGroup);
+    const long long base = (long long)C * pl.tiles;
     const long long cap = (long long)num_cu * std::max(bpc, 1);
-    const long long ckm_bytes = (long long)C * K * M * (long long)sizeof(double);
-    long long maxP = std::max(1LL, std::min(64LL, max_n / kMinSlice));
-    maxP = std::max(1LL, std::min(maxP, kPartialBytes / std::max(1LL, ckm_bytes)));
+    const long long maxP = std::max(1LL, std::min(kMaxSlices, max_n / kMinSlice));
     long long fillP = 1, wellP = 0;
     double best = -1.0;
     for (long long P = 1; P <= maxP; ++P) {
@@ -218,10 +216,14 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     return pl;
 }
 
-// S (approximate) into `S`, using `part` when the plan splits samples.
-int run_dense(dro_ctx *ctx, const dro_problem *p, const Shape &sh, double *S, double *part,
-              const DensePlan &pl, hipStream_t st)
+// Exact S into `S` ([C][K][M] doubles): the dense per-sample sums, then the
+// exact epilogue over the segments' prefix counts and sums (cnt, sum).
+int run_dense(dro_ctx *ctx, const dro_problem *p, double *S, const uint32_t *cnt,
+              const uint64_t *sum, const DensePlan &pl, hipStream_t st)
 {
+    unsigned long long *R = reinterpret_cast<unsigned long long *>(S);
+    const long long ckm = (long long)p->C * p->K * p->M;
+    HIPCHK(launch_zero_u64(R, ckm, st));
     DenseArgs a{};
     a.offsets = p->offsets;
     a.seg = p->seg;
@@ -235,20 +237,24 @@ int run_dense(dro_ctx *ctx, const dro_problem *p, const Shape &sh, double *S, do
     a.K = p->K;
     a.M = p->M;
     a.plan = pl;
-    a.out = pl.P > 1 ? part : S;
+    a.R = R;
     HIPCHK(launch_dense(a, st));
-    if (pl.P > 1) HIPCHK(launch_reduce_slices(part, pl.P, (long long)p->C * p->K * p->M, S, st));
-    (void)sh;
+    DenseFinishArgs f{};
+    f.offsets = p->offsets;
+    f.seg = p->seg;
+    f.L = p->L;
+    f.eta = p->eta;
+    f.lam = p->lam;
+    f.c_p = p->c_p;
+    f.c_w = p->c_w;
+    f.cnt = cnt;
+    f.sum = sum;
+    f.C = p->C;
+    f.K = p->K;
+    f.M = p->M;
+    f.R = R;
+    HIPCHK(launch_dense_finish(f, st));
     return DRO_OK;
-}
-
-size_t dense_bytes(const dro_problem *p, const DensePlan &pl, bool need_S)
-{
-    const size_t ckm = (size_t)p->C * p->K * p->M;
-    size_t b = 0;
-    if (need_S) b += rup(ckm * sizeof(double));
-    if (pl.P > 1) b += rup((size_t)pl.P * ckm * sizeof(double));
-    return b;
 }
 
 long long max_segment(const dro_problem *p)
@@ -581,17 +587,24 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
-    rc = ensure_ws(ctx, stage_bytes(p) + dense_bytes(p, pl, S == nullptr), st);
+    const size_t ckm = (size_t)p->C * p->K * p->M;
+    const size_t bins = (size_t)p->S * kHistBins;
+    rc = ensure_ws(ctx, stage_bytes(p) + (S ? 0 : rup(ckm * 8)) + quantile_bytes(p, ctx->num_cu) +
+                            rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    const size_t ckm = (size_t)p->C * p->K * p->M;
     double *Sbuf = S ? S : ar.take<double>(ckm);
-    double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
-    rc = run_dense(ctx, p, sh, Sbuf, part, pl, st);
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
+    uint32_t *cnt = ar.take<uint32_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
+    // the segments' value counts and sample sums, for the exact epilogue
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
+    rc = run_dense(ctx, p, Sbuf, cnt, sum, pl, st);
     if (rc) return rc;
     HIPCHK(launch_min_over_lambda(Sbuf, p->offsets, p->seg, p->lam, eps, E, p->C, p->K, p->M, W,
                                   m_star, st));
@@ -816,7 +829,8 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
-    const size_t need = dense_bytes(p, pl, true) + quantile_bytes(p, ctx->num_cu) +
+    const size_t ckm = (size_t)C * p->K * p->M;
+    const size_t need = rup(ckm * 8) + quantile_bytes(p, ctx->num_cu) +
                         refine_bytes(p, C, ctx->num_cu, false) + rup((size_t)C * 8) +
                         3 * rup((size_t)C * 4);
     rc = ensure_ws(ctx, stage_bytes(p) + need, st);
@@ -826,9 +840,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    const size_t ckm = (size_t)C * p->K * p->M;
     double *S = ar.take<double>(ckm);
-    double *part = pl.P > 1 ? ar.take<double>((size_t)pl.P * ckm) : nullptr;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     RefineBufs rb = take_refine(ar, p, C, ctx->num_cu, false);
     int64_t *q_rank = ar.take<int64_t>(C);
@@ -837,9 +849,10 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
 
     rc = run_quantile(ctx, p, qb, out->q_value, q_rank, st);
     if (rc) return rc;
-    // the quantile's value histogram also gives the prefix counts and sums of the exact argmin
+    // the quantile's value histogram also gives the prefix counts and sums of
+    // the dense epilogue and of the exact argmin
     HIPCHK(launch_prefix(qb.hist, p->S, rb.cnt, rb.sum, st));
-    rc = run_dense(ctx, p, sh, S, part, pl, st);
+    rc = run_dense(ctx, p, S, rb.cnt, rb.sum, pl, st);
     if (rc) return rc;
     HIPCHK(hipMemcpyAsync(kcur, k_prev, sizeof(int32_t) * C, hipMemcpyDeviceToDevice, st));
     for (int c = 0; c < C; ++c) {

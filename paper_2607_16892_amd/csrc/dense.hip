@@ -1,217 +1,198 @@
 // Dense evaluation of the per-sample worst-case cost and its sums
 // (paper, Appendix A, Step 4 closed form and Step 5 sums), plus the minimum
-// over the multiplier grid (the Kantorovich dual of Appendix A, Step 3, with gamma on a grid).
+// over the multiplier grid (the Kantorovich dual of Appendix A, Step 3, with
+// gamma on a grid).
 //
 // Work: one (class, grid point, multiplier, sample) term per evaluation,
 // C * K * M * N_c terms in all.  This is max-plus arithmetic, not a dense
-// contraction, so it runs on the fp32 VALU: every lane keeps a kTK x kTM
-// register tile of (grid point, multiplier) accumulators and streams the
-// samples of its class from LDS, where each tile of kTileN samples is staged
-// once per block and read back as a wave-wide broadcast.
+// contraction, so it runs on the integer VALU; there is no MFMA.
 //
-// Form of the term.  With B = c_w eta, C = c_p (L - eta), a1 = min(g, c_w) and
-// a2 = min(g, c_p), the three candidates of Step 4 reduce, for 0 <= x, eta <= L,
-// to the maximum of two lines (Q(eta, x) itself is the larger of c_w(eta - x)
-// and c_p(x - eta), and for x, L - x >= 0 the smaller slope wins each pair):
-//     phi = max(y1, y2),  y1 = B - a1 x,  y2 = C - a2 (L - x),
-// which cross at x0 = (B - C + a2 L) / (a1 + a2).  Hence, exactly,
-//     phi = y1 + (a1 + a2) relu(x - x0)      (used when c_w <= c_p)
-//     phi = y2 + (a1 + a2) relu(x0 - x)      (used when c_w >  c_p)
-// The line sums need only N and sum(x) of the slice and are formed in fp64;
-// every (c, k, m, n) term still contributes its relu, evaluated per sample.
-// The kink is measured from the grid point, x - x0 = (x - eta) - d with
-// d = x0 - eta: x - eta is an exact integer formed once per (k, sample) and
-// shared by the lane's kTM multipliers, and d is rounded to fp32 relative to
-// its own size (it is 0, hence exact, for every lam >= max(c_p, c_w)).  The
-// relu is then one instruction: u = +-(x - eta) 2^-16 plus -+d 2^-16 with the
-// [0, 1] output clamp, exact while |x - x0| < 2^16 (x0 is clamped to
-// [-1, L + 1], where relu is linear in the samples, and the clamped part is
-// added back in the epilogue).  Choosing the side of the steeper line keeps
-// the relu sum below twice the class's share of S, so the fp32 accumulation
-// carries no cancellation.  Per evaluation the inner loop is
-//     v_add_f32 t, u, a clamp ;  v_add_f32 acc, acc, t
-// two fp32 VALU instructions that gfx950 issues at the double rate, plus one
-// v_fma_f32 per (k, sample) shared by kTM evaluations.
+// Form of the term.  In units of 2^-33 (fixed.h) the three candidates of
+// Step 4 are the larger of two lines, y1 = B - A1 x and y2 = Cc - A2 (L - x),
+// whose difference is y2 - y1 = De x - Nu.  With c_w <= c_p
+//     phi = y1 + relu(De x - Nu),
+// and with t = floor(Nu / De), r = Nu - De t in [0, De), for every integer x
+//     relu(De x - Nu) = De relu(x - t) - r [x > t]
+// (x > Nu / De exactly when x > t).  With c_w > c_p the mirror image holds
+// around t = ceil(Nu / De): phi = y2 + De relu(t - x) - (De t - Nu) [x < t].
+// Summed over a class's N samples,
+//     S = sum y1 + De sum relu(x - t) - r #{x > t}
+// and  sum relu(x - t) = (sum x - N t + sum |x - t|) / 2.
+// The per-sample part of every term is |x - t|: that is what this kernel
+// evaluates, once per (c, k, m, n).  The line sums need only N and sum x, and
+// #{x > t} is one count per (c, k, m), read from the class's value counts in
+// the epilogue; every piece is an integer, so S is exact and is rounded to
+// double once.
 //
-// Accuracy: fp32 runs of kRun samples folded into fp64 in a fixed order, so
-// the result is deterministic for a given launch plan.
+// Instruction.  v_sad_u16 adds |a.lo - b.lo| + |a.hi - b.hi| (unsigned 16-bit
+// halves) to a 32-bit accumulator: with two samples x + 1 packed in a and the
+// threshold t + 1 in both halves of b, it evaluates two terms of one
+// (k, m) pair in one single-rate VALU instruction.  Samples are staged in LDS
+// as 16-bit x + 1 (x <= 2^15, t clamped to [-1, L] or [0, L + 1], so both
+// fit), read back as wave-wide broadcasts of eight samples, and every lane
+// keeps kTM thresholds and 32-bit sums of one grid point.  A 32-bit sum takes
+// at most kMaxSadSteps instructions before it is added to the 64-bit table.
+//
+// Reduction.  The samples of a class are split into P slices with their own
+// blocks; each block adds its exact integer sums to the [C][K][M] table with
+// 64-bit atomics.  Integer addition is associative, so the result does not
+// depend on the order the blocks finish in.
 #include "dro_internal.h"
+#include "fixed.h"
 
 namespace dro {
 
 __device__ __forceinline__ int seg_of(const int32_t *seg, int c) { return seg ? seg[c] : c; }
 
-// Crossing point of the two lines and the epilogue constants of one pair.
-struct PairLines {
-    double B, C, a1, a2, x0, x0c;
+// Integer threshold t of a pair and its clamp to the range a 16-bit sample
+// code can meet: [-1, L] when c_w <= c_p (relu(x - t)), [0, L + 1] otherwise
+// (relu(t - x)).  Outside those ranges the sums are linear in the samples and
+// the epilogue adds the difference.
+struct Kink {
+    int64_t t;
+    int tc;
 };
 
-__device__ __forceinline__ PairLines pair_lines(float cp, float cw, float lam, int eta, int L)
+__device__ __forceinline__ Kink pair_kink(const PairLinesFix &q, bool upper, int L)
 {
-    PairLines r;
-    const float a1 = lam < cw ? lam : cw;
-    const float a2 = lam < cp ? lam : cp;
-    r.a1 = a1;
-    r.a2 = a2;
-    r.B = (double)cw * (double)eta;
-    r.C = (double)cp * (double)(L - eta);
-    r.x0 = (r.B - r.C + (double)a2 * (double)L) / ((double)a1 + (double)a2);
-    r.x0c = r.x0 < -1.0 ? -1.0 : (r.x0 > (double)L + 1.0 ? (double)L + 1.0 : r.x0);
-    return r;
+    Kink k;
+    if (upper) {
+        k.t = floor_div(q.Nu, q.De);
+        k.tc = (int)(k.t < -1 ? -1 : (k.t > L ? L : k.t));
+    } else {
+        k.t = -floor_div(-q.Nu, q.De);
+        k.tc = (int)(k.t < 0 ? 0 : (k.t > L + 1 ? L + 1 : k.t));
+    }
+    return k;
+}
+
+// First sample (relative to the segment start) of slice p of P: even offsets,
+// so every slice but the last holds whole pairs of samples.
+__device__ __forceinline__ long long slice_start(long long N, int p, int P)
+{
+    return p >= P ? N : 2 * ((N * p) / (2LL * P));
 }
 
 __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
 {
-    __shared__ __attribute__((aligned(16))) float xs[kTileN];
-    __shared__ long long red[kThreads];
+    // The block's thresholds pass through LDS once (computed in a rolled loop),
+    // then the same memory holds the sample tiles.
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kTileN];
+    static_assert(kTileN >= kThreads * kTM, "the threshold table shares the sample tile");
 
     const DensePlan pl = a.plan;
-    // Workgroups are dispatched to the XCDs in turn (block i to XCD i mod 8), so
-    // XCD x is given one contiguous run of logical blocks; logical blocks that
-    // read the same sample slice (one class and slice, every grid and multiplier
-    // tile) are consecutive, so each slice is fetched into one XCD's L2.
+    // Workgroups are dispatched to the XCDs in turn (block i to XCD i mod 8),
+    // so XCD x is given one contiguous run of logical blocks.  Logical blocks
+    // run through a class's tiles in groups of pl.group: all P slices of one
+    // group, then the next group.  The blocks resident on an XCD at one time
+    // then read a few sample slices and add into one group's part of the
+    // table, which both stay in that XCD's L2.
     const long long nb = gridDim.x;
     const int xcd = (int)(blockIdx.x % kXcds);
-    const long long q = nb / kXcds, r = nb % kXcds;
-    long long b = xcd * q + min((long long)xcd, r) + blockIdx.x / kXcds;
-    const int tm = (int)(b % pl.tiles_m);
-    b /= pl.tiles_m;
-    const int tk = (int)(b % pl.tiles_k);
-    b /= pl.tiles_k;
-    const int p = (int)(b % pl.P);
-    b /= pl.P;
-    const int c = (int)b;
+    const long long qx = nb / kXcds, rx = nb % kXcds;
+    long long b = xcd * qx + min((long long)xcd, rx) + blockIdx.x / kXcds;
+    const long long per_class = (long long)pl.tiles * pl.P;
+    const int c = (int)(b / per_class);
+    long long rem = b % per_class;
+    const int nfull = pl.tiles / pl.group;
+    int tile, p;
+    if (rem < (long long)nfull * pl.group * pl.P) {
+        const int g = (int)(rem / ((long long)pl.group * pl.P));
+        const int r2 = (int)(rem % ((long long)pl.group * pl.P));
+        p = r2 / pl.group;
+        tile = g * pl.group + r2 % pl.group;
+    } else {
+        const int r3 = (int)(rem - (long long)nfull * pl.group * pl.P);
+        const int gl = pl.tiles - nfull * pl.group;
+        p = r3 / gl;
+        tile = nfull * pl.group + r3 % gl;
+    }
+    const int tm = tile % pl.tiles_m, tk = tile / pl.tiles_m;
 
     const int t = threadIdx.x;
     const int lm = t % pl.lanes_m, lk = t / pl.lanes_m;
-    const int BK = kTK * pl.lanes_k, BM = kTM * pl.lanes_m;
+    const int BM = kTM * pl.lanes_m;
+    const int k = tk * pl.lanes_k + lk;  // one grid point per lane
+    const int m0 = tm * BM + lm;         // multipliers m0 + j lanes_m
 
     const int s = seg_of(a.seg, c);
-    const long long n_beg = a.offsets[s], n_end = a.offsets[s + 1];
-    const long long N = n_end - n_beg;
-    const long long lo = n_beg + (N * p) / pl.P;
-    const long long hi = n_beg + (N * (p + 1)) / pl.P;
+    const long long n_beg = a.offsets[s], N = a.offsets[s + 1] - n_beg;
+    const long long lo = n_beg + slice_start(N, p, pl.P);
+    const long long hi = n_beg + slice_start(N, p + 1, pl.P);
 
-    const float cp = a.c_p[c], cw = a.c_w[c];
+    const float cpf = a.c_p[c], cwf = a.c_w[c];
+    const bool upper = cwf <= cpf;
+    const int64_t CP = fix33(cpf), CW = fix33(cwf);
     const int L = a.L[c];
-    const bool upper = cw <= cp;                          // relu on x > x0
-    const float sc = upper ? 0x1p-16f : -0x1p-16f;        // sign and scale of x - eta
+    const int eta = a.eta[min(k, a.K - 1)];
 
-    // grid point k_i = k0 + i * lanes_k, multiplier m_j = m0 + j * lanes_m
-    // (recomputed where needed rather than held in registers)
-    const int k0 = tk * BK + lk, m0 = tm * BM + lm;
-
-    float eoff[kTK];        // -+eta 2^-16
-    float add[kTK][kTM];    // -+(x0 - eta) 2^-16
+    for (int j = 0; j < kTM; ++j) {
+        const int m = min(m0 + j * pl.lanes_m, a.M - 1);
+        const PairLinesFix q = pair_lines_fix(CP, CW, fix33(a.lam[m]), eta, L);
+        xs[j * kThreads + t] = (uint16_t)(pair_kink(q, upper, L).tc + 1);
+    }
+    __syncthreads();
+    uint32_t thr[kTM];  // (t + 1) in both 16-bit halves
+    uint32_t acc[kTM];
 #pragma unroll
-    for (int i = 0; i < kTK; ++i) {
-        const int eta = a.eta[min(k0 + i * pl.lanes_k, a.K - 1)];
-        eoff[i] = -(float)eta * sc;
-#pragma unroll
-        for (int j = 0; j < kTM; ++j) {
-            const PairLines q = pair_lines(cp, cw, a.lam[min(m0 + j * pl.lanes_m, a.M - 1)], eta, L);
-            add[i][j] = -(float)(q.x0c - (double)eta) * sc;
-        }
+    for (int j = 0; j < kTM; ++j) {
+        thr[j] = (uint32_t)xs[j * kThreads + t] * 0x10001u;
+        acc[j] = 0u;
     }
 
-    double acc64[kTK][kTM];
+    const bool row_ok = k < a.K;
+    // Sample codes 0 pad the last tile to whole groups of eight; each adds
+    // t + 1 to a sum, which the flush takes off again.
+    int pads = 0, steps = 0;
+    auto flush = [&]() {
+        // Hiding the indices from the optimiser keeps it from holding the 32
+        // table addresses live across the sample loop.
+        int ke = k, me = m0;
+        asm volatile("" : "+v"(ke), "+v"(me));
+        unsigned long long *row = a.R + ((long long)c * a.K + ke) * a.M;
+        if (row_ok) {
 #pragma unroll
-    for (int i = 0; i < kTK; ++i)
+            for (int j = 0; j < kTM; ++j) {
+                const int m = me + j * pl.lanes_m;
+                if (m < a.M)
+                    atomicAdd(row + m, (unsigned long long)(acc[j] - (uint32_t)pads * (thr[j] & 0xffffu)));
+            }
+        }
 #pragma unroll
-        for (int j = 0; j < kTM; ++j) acc64[i][j] = 0.0;
+        for (int j = 0; j < kTM; ++j) acc[j] = 0u;
+        pads = 0;
+        steps = 0;
+    };
 
-    long long xsum = 0;  // this thread's share of the slice's sample sum
+    const uint4 *x4 = reinterpret_cast<const uint4 *>(xs);
     for (long long base = lo; base < hi; base += kTileN) {
         const int len = (int)min((long long)kTileN, hi - base);
+        const int len8 = (len + 7) & ~7;
+        if (steps + len8 / 2 > kMaxSadSteps) flush();
         __syncthreads();
-        for (int i = t; i < len; i += kThreads) {
-            const int x = a.xi[base + i];
-            xsum += x;
-            xs[i] = (float)x;
-        }
+        for (int i = t; i < len8; i += kThreads)
+            xs[i] = i < len ? (uint16_t)(a.xi[base + i] + 1) : (uint16_t)0;
         __syncthreads();
+        pads += len8 - len;
+        steps += len8 / 2;
 
-        for (int u0 = 0; u0 < len; u0 += kRun) {
-            const int cnt = min(kRun, len - u0);
-            // the run's first sample initialises the accumulators
-            float acc[kTK][kTM];
-            auto first = [&](float x) {
+        // eight samples per step; the next eight are read while these are summed
+        const int n4 = len8 / 8;
+        uint4 v = x4[0];
+        for (int w = 0; w < n4; ++w) {
+            const uint4 nv = x4[min(w + 1, kTileN / 8 - 1)];
 #pragma unroll
-                for (int i = 0; i < kTK; ++i) {
-                    const float u = fmaf(x, sc, eoff[i]);
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.x, thr[j], acc[j]);
 #pragma unroll
-                    for (int j = 0; j < kTM; ++j)
-                        acc[i][j] = __builtin_amdgcn_fmed3f(u + add[i][j], 0.0f, 1.0f);
-                }
-            };
-            auto step = [&](float x) {
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.y, thr[j], acc[j]);
 #pragma unroll
-                for (int i = 0; i < kTK; ++i) {
-                    const float u = fmaf(x, sc, eoff[i]);  // +-(x - eta) 2^-16, exact
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.z, thr[j], acc[j]);
 #pragma unroll
-                    for (int j = 0; j < kTM; ++j)
-                        acc[i][j] += __builtin_amdgcn_fmed3f(u + add[i][j], 0.0f, 1.0f);
-                }
-            };
-
-            first(xs[u0]);
-            int u = 1;
-            for (; u < 4 && u < cnt; ++u) step(xs[u0 + u]);
-#pragma unroll 4
-            for (; u + 4 <= cnt; u += 4) {
-                const float4 x4 = *reinterpret_cast<const float4 *>(&xs[u0 + u]);
-                step(x4.x);
-                step(x4.y);
-                step(x4.z);
-                step(x4.w);
-            }
-            for (; u < cnt; ++u) step(xs[u0 + u]);
-
-#pragma unroll
-            for (int i = 0; i < kTK; ++i)
-#pragma unroll
-                for (int j = 0; j < kTM; ++j) acc64[i][j] += (double)acc[i][j];
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.w, thr[j], acc[j]);
+            v = nv;
         }
     }
-
-    // slice sample sum (exact integer), shared by every pair of the block
-    red[t] = xsum;
-    __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
-        if (t < w) red[t] += red[t + w];
-        __syncthreads();
-    }
-    const double sx = (double)red[0];
-    const double n = (double)(hi - lo);
-
-    // The epilogue recomputes the pair constants; hiding the indices from the
-    // optimiser keeps it from holding the set-up values live across the loop.
-    int k0e = k0, m0e = m0;
-    asm volatile("" : "+v"(k0e), "+v"(m0e));
-
-    double *out = a.out + ((long long)p * a.C + c) * (long long)a.K * a.M;
-#pragma unroll
-    for (int i = 0; i < kTK; ++i) {
-        const int k = k0e + i * pl.lanes_k;
-        if (k >= a.K) continue;
-        const int eta = a.eta[k];
-#pragma unroll
-        for (int j = 0; j < kTM; ++j) {
-            const int m = m0e + j * pl.lanes_m;
-            if (m >= a.M) continue;
-            const PairLines q = pair_lines(cp, cw, a.lam[m], eta, L);
-            const double relu = acc64[i][j] * 65536.0;
-            double line, corr = 0.0;
-            if (upper) {
-                line = n * q.B - q.a1 * sx;
-                if (q.x0 < q.x0c) corr = n * (q.x0c - q.x0);
-            } else {
-                line = n * (q.C - q.a2 * (double)L) + q.a2 * sx;
-                if (q.x0 > q.x0c) corr = n * (q.x0 - q.x0c);
-            }
-            out[(long long)k * a.M + m] = line + (q.a1 + q.a2) * (relu + corr);
-        }
-    }
+    if (steps > 0) flush();
 }
 
 int dense_blocks_per_cu()
@@ -228,19 +209,71 @@ hipError_t launch_dense(const DenseArgs &a, hipStream_t st)
     return hipGetLastError();
 }
 
-__global__ void reduce_slices_kernel(const double *part, int P, long long n, double *S)
+__global__ void fill_u64_kernel(unsigned long long *p, long long n)
 {
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    double acc = 0.0;
-    for (int p = 0; p < P; ++p) acc += part[(long long)p * n + i];
-    S[i] = acc;
+    if (i < n) p[i] = 0ull;
 }
 
-hipError_t launch_reduce_slices(const double *part, int P, long long n, double *S, hipStream_t st)
+hipError_t launch_zero_u64(unsigned long long *p, long long n, hipStream_t st)
 {
-    const long long blocks = (n + 255) / 256;
-    hipLaunchKernelGGL(reduce_slices_kernel, dim3((unsigned)blocks), dim3(256), 0, st, part, P, n, S);
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_u64_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n);
+    return hipGetLastError();
+}
+
+// #{x <= v} of a segment from its prefix counts (cn[v], v in [0, 2^15]).
+__device__ __forceinline__ long long count_le(const uint32_t *cn, long long v, long long N)
+{
+    if (v < 0) return 0;
+    if (v >= kHistBins - 1) return N;
+    return (long long)cn[v];
+}
+
+// S[c,k,m] from the per-sample sums sum |x - t_c| of the dense kernel (in R,
+// overwritten in place), the segment's value counts and its sample sum:
+// exactly, in 128-bit integers in units of 2^-33, then rounded to double once.
+__global__ void dense_finish_kernel(DenseFinishArgs a)
+{
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long long KM = (long long)a.K * a.M;
+    if (i >= (long long)a.C * KM) return;
+    const int c = (int)(i / KM);
+    const int k = (int)((i / a.M) % a.K);
+    const int m = (int)(i % a.M);
+    const int s = seg_of(a.seg, c);
+    const long long N = a.offsets[s + 1] - a.offsets[s];
+    const uint32_t *cn = a.cnt + (long long)s * kHistBins;
+    const __int128 sx = (__int128)a.sum[(long long)s * kHistBins + kHistBins - 1];
+    const float cpf = a.c_p[c], cwf = a.c_w[c];
+    const bool upper = cwf <= cpf;
+    const int L = a.L[c];
+    const PairLinesFix q = pair_lines_fix(fix33(cpf), fix33(cwf), fix33(a.lam[m]), a.eta[k], L);
+    const Kink kk = pair_kink(q, upper, L);
+    const __int128 sad = (__int128)a.R[i];
+    const __int128 n = N, tc = kk.tc, tt = kk.t;
+    __int128 S;
+    if (upper) {
+        // sum relu(x - t) with the clamp undone for t < -1 (every sample above t)
+        const __int128 Rt = (sx - n * tc + sad) / 2 + n * (tc > tt ? tc - tt : 0);
+        const __int128 r = (__int128)q.Nu - (__int128)q.De * tt;
+        const __int128 above = n - count_le(cn, kk.t, N);
+        S = n * q.B - (__int128)q.A1 * sx + (__int128)q.De * Rt - r * above;
+    } else {
+        // sum relu(t - x) with the clamp undone for t > L + 1 (every sample below t)
+        const __int128 Rt = (n * tc - sx + sad) / 2 + n * (tt > tc ? tt - tc : 0);
+        const __int128 r = (__int128)q.De * tt - (__int128)q.Nu;
+        const __int128 below = count_le(cn, kk.t - 1, N);
+        S = n * ((__int128)q.Cc - (__int128)q.A2 * L) + (__int128)q.A2 * sx + (__int128)q.De * Rt -
+            r * below;
+    }
+    reinterpret_cast<double *>(a.R)[i] = sfix128_to_double(S);
+}
+
+hipError_t launch_dense_finish(const DenseFinishArgs &a, hipStream_t st)
+{
+    const long long n = (long long)a.C * a.K * a.M;
+    hipLaunchKernelGGL(dense_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 

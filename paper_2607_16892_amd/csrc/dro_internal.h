@@ -10,21 +10,24 @@
 namespace dro {
 
 // ---- dense evaluation -------------------------------------------------------
-// Every lane owns a register tile of kTK grid points x kTM multipliers; a
-// 256-lane block covers (TK * lanes_k) x (TM * lanes_m) pairs of one class and
-// one slice of that class's samples, staged through LDS.
+// Every lane owns one grid point and kTM multipliers; a 256-lane block covers
+// lanes_k x (kTM * lanes_m) pairs of one class and one slice of that class's
+// samples, staged through LDS as 16-bit codes x + 1.
 constexpr int kThreads = 256;
-constexpr int kTK = 1;
 constexpr int kTM = 32;
-constexpr int kTileN = 1024;  // samples staged per LDS tile
-constexpr int kRun = 64;      // fp32 run length before the fp64 fold
-constexpr int kXcds = 8;      // accelerator complex dies of one MI355X (one L2 each)
+constexpr int kTileN = 8192;          // samples staged per LDS tile (a multiple of 8)
+constexpr int kMaxSadSteps = 65532;   // v_sad_u16 steps per 32-bit sum: each adds at most
+                                      // 2 * 32770, and 65532 * 65540 < 2^32
+constexpr int kXcds = 8;              // accelerator complex dies of one MI355X (one L2 each)
+constexpr int kTileGroup = 32;        // tiles whose slices run together (block order)
 
 struct DensePlan {
     int lanes_m, lanes_k;  // lane grid inside a block
     int tiles_k, tiles_m;  // block tiles per class
+    int tiles;             // tiles_k * tiles_m
+    int group;             // tiles per group of the block order, <= tiles
     int P;                 // sample slices per class
-    long long blocks;      // C * tiles_k * tiles_m * P
+    long long blocks;      // C * tiles * P
 };
 
 struct DenseArgs {
@@ -38,14 +41,30 @@ struct DenseArgs {
     const float *c_w;
     int C, K, M;
     DensePlan plan;
-    double *out;  // [P][C][K][M]; with P == 1 this is S itself
+    unsigned long long *R;  // [C][K][M] sums of |x - t| over the class's samples, zeroed first
 };
 
 hipError_t launch_dense(const DenseArgs &a, hipStream_t st);
 // resident dense blocks per compute unit (occupancy of dense_kernel)
 int dense_blocks_per_cu();
-// S[i] = sum_p part[p * n + i], p ascending
-hipError_t launch_reduce_slices(const double *part, int P, long long n, double *S, hipStream_t st);
+hipError_t launch_zero_u64(unsigned long long *p, long long n, hipStream_t st);
+
+// S from the dense kernel's sums and the segments' prefix counts and sums
+// (cnt, sum: [S][kHistBins], from launch_prefix), written over R as doubles.
+struct DenseFinishArgs {
+    const int64_t *offsets;
+    const int32_t *seg;
+    const int32_t *L;
+    const int32_t *eta;
+    const float *lam;
+    const float *c_p;
+    const float *c_w;
+    const uint32_t *cnt;
+    const uint64_t *sum;
+    int C, K, M;
+    unsigned long long *R;
+};
+hipError_t launch_dense_finish(const DenseFinishArgs &a, hipStream_t st);
 // W[e,c,k] = min_m RN(RN(lam_m eps[e,c]) + RN(S[c,k,m] / N_c)), lowest m
 hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const int32_t *seg,
                                   const float *lam, const float *eps, int E, int C, int K, int M,

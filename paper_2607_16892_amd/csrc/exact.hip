@@ -13,6 +13,7 @@
 #include <algorithm>
 
 #include "dro_internal.h"
+#include "fixed.h"
 
 namespace dro {
 
@@ -23,16 +24,6 @@ __device__ __forceinline__ int seg_of_x(const int32_t *seg, int c) { return seg 
         const hipError_t e_ = (expr);                \
         if (e_ != hipSuccess) return e_;             \
     } while (0)
-
-// v * 2^33 for a binary32 v in [2^-10, 2^7] (exact integer below 2^41).
-__device__ __forceinline__ int64_t fix33(float v)
-{
-    const uint32_t bits = __float_as_uint(v);
-    const int e = (int)((bits >> 23) & 0xffu);
-    const int64_t mant = (int64_t)((bits & 0x7fffffu) | 0x800000u);
-    const int sh = e - 117;  // e - 127 - 23 + 33
-    return sh >= 0 ? (mant << sh) : (mant >> (-sh));
-}
 
 // phi in units of 2^-33: the three candidate points 0, x and L of Step 4.
 __device__ __forceinline__ int64_t phi_fix(int64_t eta, int64_t x, int64_t L, int64_t CP,
@@ -46,38 +37,11 @@ __device__ __forceinline__ int64_t phi_fix(int64_t eta, int64_t x, int64_t L, in
     return q_x > m ? q_x : m;
 }
 
-// Correctly rounded double of the unsigned 128-bit value (hi, lo) times 2^-33.
-__device__ double fix128_to_double(uint64_t lo, uint64_t hi)
-{
-    int nb;
-    if (hi) nb = 128 - __clzll((long long)hi);
-    else if (lo) nb = 64 - __clzll((long long)lo);
-    else return 0.0;
-    if (nb <= 53) return ldexp((double)(long long)lo, -33);
-    const int sh = nb - 53;
-    const unsigned __int128 v = ((unsigned __int128)hi << 64) | (unsigned __int128)lo;
-    uint64_t mant = (uint64_t)(v >> sh);
-    const unsigned __int128 rem = v & ((((unsigned __int128)1) << sh) - 1);
-    const unsigned __int128 half = ((unsigned __int128)1) << (sh - 1);
-    if (rem > half || (rem == half && (mant & 1u))) mant += 1;
-    return ldexp((double)(long long)mant, sh - 33);
-}
-
 __device__ __forceinline__ void add128(uint64_t &lo, uint64_t &hi, uint64_t blo, uint64_t bhi)
 {
     const uint64_t r = lo + blo;
     hi += bhi + (r < lo ? 1u : 0u);
     lo = r;
-}
-
-// floor(a / b) for b > 0 and |a| < 2^62: a double estimate (within 1 of the
-// quotient for the ranges used here) corrected with exact integer products.
-__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)
-{
-    int64_t q = (int64_t)floor((double)a / (double)b);
-    while (q * b > a) --q;
-    while ((q + 1) * b <= a) ++q;
-    return q;
 }
 
 // Exact S of one (class, grid point, multiplier), in units of 2^-33, from the
