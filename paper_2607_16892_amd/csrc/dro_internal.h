@@ -19,7 +19,7 @@ constexpr int kTileN = 8192;          // samples staged per LDS tile (a multiple
 constexpr int kMaxSadSteps = 65532;   // v_sad_u16 steps per 32-bit sum: each adds at most
                                       // 2 * 32770, and 65532 * 65540 < 2^32
 constexpr int kXcds = 8;              // accelerator complex dies of one MI355X (one L2 each)
-constexpr int kTileGroup = 32;        // tiles whose slices run together (block order)
+constexpr int kTileGroup = 64;        // tiles whose slices run together (block order)
 
 struct DensePlan {
     int lanes_m, lanes_k;  // lane grid inside a block
