@@ -149,6 +149,25 @@ int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out);
 int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps, double *W,
                   int32_t *m_star, double *S, dro_stream_t stream);
 
+/* Bytes of the device array that dro_cost_eval_noalloc takes its scratch from
+ * (one array per device, held until the process ends). */
+#define DRO_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* dro_cost_eval for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, results and errors as dro_cost_eval, except that S is
+ * required (the dense sums accumulate in it) and the scratch (the staged
+ * offsets and segment map, the value histogram, the prefix counts and sums)
+ * comes from a static device array of DRO_NOALLOC_SCRATCH_BYTES instead of
+ * the ctx workspace, so the call allocates nothing.  The scratch grows with
+ * the number of sample segments, about 0.5 MB each: a problem that needs
+ * more than the array (beyond about 60 segments) gets DRO_ELIMIT before any
+ * work is enqueued.  Every call on one device shares that device's array and
+ * leaves its contents behind; two calls that overlap on one device (from
+ * different streams or host threads) race. */
+int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
+                          double *W, int32_t *m_star, double *S, dro_stream_t stream);
+
 /* Optimal grid reservation per (e, c) (Prop. 4.2 on the grid):
  *   k_star[e,c]    = lowest k <= k_max[c] minimising min_m J   (k_max NULL = K-1)
  *   W_star[e,c]    = exact J at the optimum: J = RN(RN(lam eps) + RN(RN(S)/N)) with S

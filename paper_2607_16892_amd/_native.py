@@ -45,6 +45,7 @@ EXPORTS = {
     "dro_validate": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P]),
     "dro_take_flags": (ct.c_int, [P, ct.POINTER(ct.c_uint32)]),
     "dro_cost_eval": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P]),
+    "dro_cost_eval_noalloc": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P]),
     "dro_argmin_reservation": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P, P, P]),
     "class_quantile": (ct.c_int, [P, ct.POINTER(ProblemStruct), P, P, P]),
     "dro_exact_table": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P, P, P, P]),

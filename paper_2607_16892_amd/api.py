@@ -210,6 +210,27 @@ def dro_cost_eval(ctx: Context, prob: Problem, eps: torch.Tensor, W=None, m_star
     return dict(W=W, m_star=m_star, S=S)
 
 
+def dro_cost_eval_noalloc(ctx: Context, prob: Problem, eps: torch.Tensor, S: torch.Tensor,
+                          W: torch.Tensor, m_star: Optional[torch.Tensor] = None,
+                          stream=None) -> dict:
+    """dro_cost_eval with the library's static scratch array (see dro_cost_eval_noalloc in
+    dro.h): every output is the caller's, S included."""
+    dev = prob.device
+    _need_dev(eps, torch.float32, "eps", dev)
+    E = eps.numel() // prob.C
+    if E * prob.C != eps.numel() or E <= 0:
+        raise ValueError("eps must hold E*C radii")
+    S = _out(S, (prob.C, prob.K, prob.M), torch.float64, dev, "S")
+    W = _out(W, (E, prob.C, prob.K), torch.float64, dev, "W")
+    if m_star is not None:
+        m_star = _out(m_star, (E, prob.C, prob.K), torch.int32, dev, "m_star")
+    ps = prob.struct()
+    rc = ctx._lib.dro_cost_eval_noalloc(ctx.handle, ct.byref(ps), E, _ptr(eps), _ptr(W),
+                                        _ptr(m_star), _ptr(S), _stream(stream, dev))
+    ctx.check(rc, "dro_cost_eval_noalloc")
+    return dict(W=W, m_star=m_star, S=S)
+
+
 def dro_argmin_reservation(ctx: Context, prob: Problem, eps: torch.Tensor, S: torch.Tensor,
                            k_max: Optional[torch.Tensor] = None, k_star=None, W_star=None,
                            m_at_star=None, stream=None) -> dict:

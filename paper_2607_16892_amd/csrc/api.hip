@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "dro_internal.h"
@@ -17,6 +18,7 @@ struct dro_ctx {
     void *ws = nullptr;
     size_t ws_size = 0;
     uint32_t *flags = nullptr;  // device word of DRO_FLAG_* bits
+    void *scratch = nullptr;    // device address of this device's no-allocation scratch array
     char err[1024] = {0};
     // host staging of the configuration-space count table (kept alive until
     // the next configuration search on this context has been enqueued)
@@ -24,9 +26,34 @@ struct dro_ctx {
     std::vector<int32_t> gpus_h;
 };
 
+// Scratch of dro_cost_eval_noalloc: a fixed array in every device's memory,
+// held until the process ends.  Host code never uses its name as an address:
+// the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[DRO_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 using namespace dro;
+
+std::mutex g_scratch_mu;
+std::vector<void *> g_scratch_ptr;  // indexed by HIP device
+
+// The device address of `scratch` on the current device `dev` (looked up on
+// the first call for that device).
+hipError_t scratch_address(int dev, void **out)
+{
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
 
 int fail(dro_ctx *ctx, int code, const char *fmt, ...)
 {
@@ -279,6 +306,15 @@ size_t quantile_bytes(const dro_problem *p, int num_cu)
     return rup((size_t)p->S * kHistBins * 4) + (B > 1 ? rup((size_t)p->S * B * kHistBins * 4) : 0);
 }
 
+QuantBufs take_quantile_parts(Arena &ar, const dro_problem *p, int B)
+{
+    QuantBufs q;
+    q.B = B;
+    q.hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
+    q.part = q.B > 1 ? ar.take<uint32_t>((size_t)p->S * q.B * kHistBins) : nullptr;
+    return q;
+}
+
 QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
 {
     QuantBufs q;
@@ -427,6 +463,39 @@ int check_rows(dro_ctx *ctx, int E, int C)
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 bool in_limits(float v) { return v >= 0x1p-10f && v <= 0x1p7f; }
 
+// Scratch of one dense evaluation beyond S: the staged offsets and segment
+// map, the value histogram with B parts per segment, the prefix counts and sums.
+size_t cost_eval_scratch_bytes(const dro_problem *p, int B)
+{
+    const size_t bins = (size_t)p->S * kHistBins;
+    return stage_bytes(p) + rup(bins * 4) + (B > 1 ? rup(bins * B * 4) : 0) + rup(bins * 4) +
+           rup(prefix_sum_words(p->S) * 8);
+}
+
+// The dense evaluation over scratch taken from `ar` (the device must be
+// current): value counts and sample sums of every segment, the exact S into
+// Sbuf, then the minimum over the multipliers.
+int run_cost_eval(dro_ctx *ctx, const dro_problem *p, const Shape &sh, int E, const float *eps,
+                  double *W, int32_t *m_star, double *Sbuf, Arena &ar, int B, hipStream_t st)
+{
+    dro_problem q;
+    int rc = stage_problem(ctx, p, ar, st, &q);
+    if (rc) return rc;
+    p = &q;
+    const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
+    const size_t bins = (size_t)p->S * kHistBins;
+    const QuantBufs qb = take_quantile_parts(ar, p, B);
+    uint32_t *cnt = ar.take<uint32_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
+    rc = run_dense(ctx, p, Sbuf, cnt, sum, pl, st);
+    if (rc) return rc;
+    HIPCHK(launch_min_over_lambda(Sbuf, p->offsets, p->seg, p->lam, eps, E, p->C, p->K, p->M, W,
+                                  m_star, st));
+    return DRO_OK;
+}
+
 }  // namespace
 
 // ============================================================== C ABI ====
@@ -465,6 +534,11 @@ int dro_create(int hip_device, dro_ctx **out)
         (void)hipGetLastError();
         delete ctx;
         return DRO_EHIP;
+    }
+    // the no-allocation entry point reports DRO_EHIP if this lookup failed
+    if (scratch_address(hip_device, &ctx->scratch) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->scratch = nullptr;
     }
     if (hipMalloc(&ctx->flags, sizeof(uint32_t)) != hipSuccess) {
         (void)hipGetLastError();
@@ -589,29 +663,40 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     if ((rc = check_rows(ctx, E, p->C))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const size_t ckm = (size_t)p->C * p->K * p->M;
-    const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + (S ? 0 : rup(ckm * 8)) + quantile_bytes(p, ctx->num_cu) +
-                            rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
+    const int B = hist_parts(p->S, max_segment(p), ctx->num_cu);
+    rc = ensure_ws(ctx, (S ? 0 : rup(ckm * 8)) + cost_eval_scratch_bytes(p, B), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
-    dro_problem q;
-    rc = stage_problem(ctx, p, ar, st, &q);
-    if (rc) return rc;
-    p = &q;
     double *Sbuf = S ? S : ar.take<double>(ckm);
-    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
-    uint32_t *cnt = ar.take<uint32_t>(bins);
-    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
-    // the segments' value counts and sample sums, for the exact epilogue
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
-    HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
-    rc = run_dense(ctx, p, Sbuf, cnt, sum, pl, st);
+    return run_cost_eval(ctx, p, sh, E, eps, W, m_star, Sbuf, ar, B, st);
+}
+
+int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
+                          double *W, int32_t *m_star, double *S, dro_stream_t stream)
+{
+    Shape sh;
+    int rc = check_problem(ctx, p, &sh);
     if (rc) return rc;
-    HIPCHK(launch_min_over_lambda(Sbuf, p->offsets, p->seg, p->lam, eps, E, p->C, p->K, p->M, W,
-                                  m_star, st));
-    return DRO_OK;
+    if (E <= 0 || !eps || !W || !S)
+        return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W, S non-NULL");
+    if ((rc = check_rows(ctx, E, p->C))) return rc;
+    if (!ctx->scratch)
+        return fail(ctx, DRO_EHIP, "the scratch array's device address is unknown on device %d",
+                    ctx->device);
+    // as many histogram parts as the array leaves room for (at most the
+    // workspace path's), down to one
+    const size_t cap = DRO_NOALLOC_SCRATCH_BYTES;
+    const size_t need1 = cost_eval_scratch_bytes(p, 1);
+    if (need1 > cap)
+        return fail(ctx, DRO_ELIMIT,
+                    "the problem needs %zu bytes of scratch; the no-allocation array holds %zu",
+                    need1, cap);
+    int B = hist_parts(p->S, max_segment(p), ctx->num_cu);
+    while (B > 1 && cost_eval_scratch_bytes(p, B) > cap) --B;
+    ENTER_DEVICE(ctx);
+    Arena ar{(char *)ctx->scratch, 0};
+    return run_cost_eval(ctx, p, sh, E, eps, W, m_star, S, ar, B, (hipStream_t)stream);
 }
 
 int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
