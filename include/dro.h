@@ -42,8 +42,8 @@
  *    K <= 2^15 + 1 grid points, M <= 65536 multipliers, K * M < 2^31 pairs
  *    and E * C < 2^31 radius rows.
  *    Inside them every candidate of phi is a multiple of 2^-33 below 2^56, so
- *    the library can evaluate S exactly in 128-bit fixed point where the
- *    result is an index (argmin, quantile) or the reported optimum.
+ *    the library evaluates every S exactly in 128-bit fixed point and rounds
+ *    it to double once.
  *
  * Layout: tables are row-major, class-major:
  *    S      [C][K][M]      fp64
@@ -137,15 +137,17 @@ int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out);
 
 /* Dense evaluation (Appendix A, Steps 4-5) and the minimum over the
  * multiplier grid (Kantorovich dual, Appendix A, Step 3):
- *   S[c,k,m]  = sum over the samples of class c of phi(eta_k, x, lam_m)
- *               every (c,k,m,n) term in fp32, runs of at most 64 samples
- *               folded into fp64 in a fixed order (deterministic)
+ *   S[c,k,m]  = sum over the samples of class c of phi(eta_k, x, lam_m), exactly:
+ *               every (c,k,m,n) term's per-sample part |x - t| (t the integer
+ *               floor or ceiling of the crossing point of phi's two lines) is
+ *               summed in integers on the GPU, and the rest of each term follows
+ *               from N, the sample sum and one value count per (c,k,m); S is the
+ *               correctly rounded double of the exact sum (deterministic)
  *   W[e,c,k]  = min over m of  RN(RN(lam_m eps[e,c]) + RN(S[c,k,m] / N_c))
  *   m_star    = the lowest m attaining it.
- * S may be NULL (kept in the ctx workspace); m_star may be NULL.
- * W is within 1e-5 relative of its exact value (typically about 1e-7; 2e-6
- * when every sample sits at the kink of phi); use dro_argmin_reservation for
- * the exact optimum. */
+ * S may be NULL (kept in the ctx workspace); m_star may be NULL.  Inside the
+ * exactness limits S, W and m_star are exact for every cost ratio: the same
+ * values as the exact-spec expression of dro_argmin_reservation. */
 int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps, double *W,
                   int32_t *m_star, double *S, dro_stream_t stream);
 
@@ -178,8 +180,9 @@ int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const f
  * minimum, at most 256 per (e, c)), which are then evaluated exactly.  Where
  * the band overflows or the exact optimum sits near its edge, the exact table
  * of dro_exact_table settles that (e, c) instead and a DRO_FLAG_* bit is
- * raised; the result is exact either way.  Ties go to the lowest k, then the
- * lowest m. */
+ * raised; the result is exact either way (and since dro_cost_eval's S is
+ * exact, the screen can only miss through an overflowing band).  Ties go to
+ * the lowest k, then the lowest m. */
 int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
                            const double *S, const int32_t *k_max, int32_t *k_star, double *W_star,
                            int32_t *m_at_star, dro_stream_t stream);

@@ -60,6 +60,8 @@ def _load():
             lib.oracle_S_exact_at.argtypes = [i32, P, P, P, P, P, P, P, P, i32, P, P, P, P, P]
             lib.oracle_fix_to_double.restype = ct.c_double
             lib.oracle_fix_to_double.argtypes = [i64, ct.c_uint64]
+            lib.oracle_fix_to_double_n.restype = None
+            lib.oracle_fix_to_double_n.argtypes = [i64, P, P, P]
             lib.oracle_J.restype = ct.c_double
             lib.oracle_J.argtypes = [i64, ct.c_uint64, f32, f32, i64]
             lib.oracle_W.restype = None
@@ -137,11 +139,10 @@ class ExactS:
         return (int(self.hi[idx]) << 64) | int(self.lo[idx])
 
     def to_double(self) -> np.ndarray:
-        lib = _load()
-        out = np.empty(self.hi.shape, np.float64)
-        h, l, o = self.hi.reshape(-1), self.lo.reshape(-1), out.reshape(-1)
-        for i in range(h.size):
-            o[i] = lib.oracle_fix_to_double(int(h[i]), int(l[i]))
+        h = np.ascontiguousarray(self.hi, np.int64)
+        l = np.ascontiguousarray(self.lo, np.uint64)
+        out = np.empty(h.shape, np.float64)
+        _load().oracle_fix_to_double_n(h.size, _p(h), _p(l), _p(out))
         return out
 
 

@@ -234,6 +234,12 @@ double oracle_fix_to_double(int64_t hi, uint64_t lo)
     return ldexp((double)v, -FIX_SHIFT);
 }
 
+/* out[i] = RN64 of (hi[i], lo[i]) for n values (oracle_fix_to_double over an array). */
+void oracle_fix_to_double_n(int64_t n, const int64_t *hi, const uint64_t *lo, double *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_fix_to_double(hi[i], lo[i]);
+}
+
 /* J = RN(RN(lam*eps) + RN(RN(S)/N)); lam*eps is exact in double. */
 double oracle_J(int64_t hi, uint64_t lo, float lam, float eps, int64_t N)
 {

@@ -311,6 +311,45 @@ def test_P12_grouped_equals_per_sample():
     assert np.array_equal(a.hi, b.hi) and np.array_equal(a.lo, b.lo)
 
 
+def test_P12_exact_at_equals_the_full_exact_sums():
+    """oracle_S_exact_at (the reference of every full-size spot check of S)
+    against the full per-sample and value-grouped sums at 300 random
+    (c, k, m): aliased segments, a segment of one sample, K, M > 1."""
+    w = random_workload(seed=71, C=7, N=(1, 250, 37, 900), alias=True, L=3000, K=41, M=23, E=1)
+    assert w.seg is not None and min(np.diff(w.offsets)) == 1
+    full = oracle.S_exact(w, grouped=False)
+    grouped = oracle.S_exact(w, grouped=True)
+    rng = np.random.default_rng(0)
+    cs, ks, ms = rng.integers(0, w.C, 300), rng.integers(0, w.K, 300), rng.integers(0, w.M, 300)
+    cs[:4] = [c for c in range(w.C) if w.seg[c] == 0][:1] * 4     # the one-sample segment
+    at = oracle.S_exact_at(w, cs, ks, ms)
+    for i, (c, k, m) in enumerate(zip(cs, ks, ms)):
+        assert at.as_int(i) == full.as_int((c, k, m)) == grouped.as_int((c, k, m)), (c, k, m)
+
+
+def test_P12_exact_at_equals_the_scanned_supremum_summed_in_rationals():
+    """oracle_S_exact_at against the sum over the samples of the supremum of
+    Step 4 found by scanning the support (brute.sup_brute), in rationals."""
+    w = _tiny(72, C=3, N=(5, 1, 8), L=60, K=7, M=5)
+    rng = np.random.default_rng(1)
+    cs, ks, ms = rng.integers(0, w.C, 24), rng.integers(0, w.K, 24), rng.integers(0, w.M, 24)
+    at = oracle.S_exact_at(w, cs, ks, ms)
+    for i, (c, k, m) in enumerate(zip(cs, ks, ms)):
+        xs = w.samples_of(int(c))
+        want = sum((brute.sup_brute(int(w.eta[k]), int(x), int(w.L[c]), float(w.c_p[c]),
+                                    float(w.c_w[c]), float(w.lam[m])) for x in xs), F(0))
+        assert F(at.as_int(i), 1 << 33) == want, (c, k, m)
+
+
+def test_fix_to_double_array_equals_the_scalar():
+    rng = np.random.default_rng(4)
+    hi = rng.integers(0, 1 << 20, 500).astype(np.int64)
+    lo = rng.integers(0, 1 << 63, 500, dtype=np.uint64) * np.uint64(2) + np.uint64(1)
+    got = oracle.ExactS(hi, lo).to_double()
+    for i in range(500):
+        assert got[i] == oracle._load().oracle_fix_to_double(int(hi[i]), int(lo[i]))
+
+
 def test_fix_to_double_is_correctly_rounded():
     rng = np.random.default_rng(3)
     for _ in range(2000):
