@@ -243,6 +243,12 @@ def _drift_base():
     return base, cps, cap, conc
 
 
+def drift_base_draws() -> list:
+    """The fixed per-class draws of drift-8x4M before rounding: iteration t
+    holds clip(rint(draw * 1.01**t), 1, 32768) of each (fp64 throughout)."""
+    return _drift_base()[0]
+
+
 def _drift_8x4M(iteration: int = 0) -> Workload:
     base, cps, cap, conc = _drift_base()
     L, C = 32768, 8
