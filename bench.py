@@ -201,7 +201,6 @@ def bench_bcd(ctx, dev, iters: int):
         k = o["k_next"]
         usage = o["usage"].cpu().numpy()
         binding = int((usage > 0.98 * w0.groups.cap).sum())
-    flags = ctx.take_flags()
     ms = float(np.median(times)) if times else None
     return dict(workload="drift-8x4M: 8 classes x 4e6 lognormal drifting 1%/iteration, K=2048, "
                          "M=256, G=6",
@@ -209,7 +208,7 @@ def bench_bcd(ctx, dev, iters: int):
                 ms_max=float(np.max(times)) if times else None,
                 ms_total=float(np.sum(times)), evals_per_iter=w0.evals,
                 evals_per_s=(w0.evals / (ms / 1e3)) if ms else None,
-                binding_groups_last_iter=binding, k_final=k.cpu().tolist(), flags=flags,
+                binding_groups_last_iter=binding, k_final=k.cpu().tolist(),
                 generator_check=checked)
 
 
@@ -397,7 +396,6 @@ def main():
         step(pairs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    flags = ctx.take_flags()
     ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
     launch_times = [e[1].elapsed_time(e[2]) for e in pairs]
     dense_ms = float(np.mean(launch_times))
@@ -409,7 +407,7 @@ def main():
     evals = w.evals
     value = evals / (ms_step / 1e3)
     dense_rate = evals / (dense_ms / 1e3)
-    _log(f"step {ms_step:.2f} ms, dense {dense_ms:.2f} ms, {value:.3e} evals/s, flags={flags}")
+    _log(f"step {ms_step:.2f} ms, dense {dense_ms:.2f} ms, {value:.3e} evals/s")
     cnt = _counters_for(w.name)
 
     # Exact table from value counts (not the per-term metric; reported beside it)
@@ -536,7 +534,6 @@ def main():
                                 "sums in 128-bit integers; it does not evaluate per-sample terms, "
                                 "so it is reported beside the metric, not as it",
                         "equivalent_evals_per_s": evals / (exact_ms / 1e3)},
-        "flags": flags,
         "platform": _platform(dev),
     }
     print(json.dumps(line), flush=True)

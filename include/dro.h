@@ -27,9 +27,8 @@
  *    caller pointer after the call returns; scratch memory belongs to the ctx.
  *  - Every compute call is asynchronous on `stream` (a hipStream_t; NULL is
  *    the null stream): it returns after enqueueing, outputs are valid after
- *    the stream is synchronised.  dro_validate, dro_take_flags and
- *    dro_bcd_solve (whose loop reads its decisions on the host) are
- *    synchronous.
+ *    the stream is synchronised.  dro_validate and dro_bcd_solve (whose loop
+ *    reads its decisions on the host) are synchronous.
  *  - Return value 0 = DRO_OK, negative = error.  Nothing is thrown across the
  *    ABI.  On an error found on the host no kernel is launched and no output
  *    is written; dro_last_error(ctx) holds the detail.
@@ -70,15 +69,6 @@ enum {
     DRO_ENOMEM = -3, /* workspace allocation failed                                      */
     DRO_EHIP = -4,   /* HIP runtime error; dro_last_error keeps its text                 */
     DRO_ELIMIT = -5  /* beyond the exactness limits above                                */
-};
-
-/* Status bits accumulated on the device by the exact argmin; read and
- * cleared with dro_take_flags.  They report how an optimum was found, not an
- * error: where the screening band did not settle it, the exact table of that
- * (e, c) did, and the result is the same exact optimum either way. */
-enum {
-    DRO_FLAG_BAND_FULL = 1u,   /* a screening band held more candidates than it keeps (256)   */
-    DRO_FLAG_BAND_MARGIN = 2u  /* the exact optimum sat too close to the band edge            */
 };
 
 /* The reservation sub-problem of one set of classes (paper, Sec. 3.4 and
@@ -132,9 +122,6 @@ const char *dro_last_error(const dro_ctx *ctx);
 int dro_validate(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
                  dro_stream_t stream);
 
-/* Read and clear the DRO_FLAG_* bits raised since the last call (synchronous). */
-int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out);
-
 /* Dense evaluation (Appendix A, Steps 4-5) and the minimum over the
  * multiplier grid (Kantorovich dual, Appendix A, Step 3):
  *   S[c,k,m]  = sum over the samples of class c of phi(eta_k, x, lam_m), exactly:
@@ -171,18 +158,12 @@ int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const f
                           double *W, int32_t *m_star, double *S, dro_stream_t stream);
 
 /* Optimal grid reservation per (e, c) (Prop. 4.2 on the grid):
- *   k_star[e,c]    = lowest k <= k_max[c] minimising min_m J   (k_max NULL = K-1)
- *   W_star[e,c]    = exact J at the optimum: J = RN(RN(lam eps) + RN(RN(S)/N)) with S
- *                    the exact sum of phi (128-bit fixed point), round-to-nearest-even
+ *   k_star[e,c]    = lowest k <= k_max[c] minimising W[e,c,k] = min_m J   (k_max NULL = K-1)
+ *   W_star[e,c]    = J at the optimum: J = RN(RN(lam eps) + RN(S/N)), round-to-nearest-even
  *   m_at_star[e,c] = lowest m attaining it (may be NULL).
- * `S` is the table written by dro_cost_eval for the same problem; it is used to
- * screen candidates (every (k, m) within 1e-4 relative of the screened
- * minimum, at most 256 per (e, c)), which are then evaluated exactly.  Where
- * the band overflows or the exact optimum sits near its edge, the exact table
- * of dro_exact_table settles that (e, c) instead and a DRO_FLAG_* bit is
- * raised; the result is exact either way (and since dro_cost_eval's S is
- * exact, the screen can only miss through an overflowing band).  Ties go to
- * the lowest k, then the lowest m. */
+ * `S` is the table written by dro_cost_eval for the same problem: the
+ * correctly rounded double of the exact sum, so every J is the exact-spec
+ * value and the optimum is exact.  Ties go to the lowest k, then the lowest m. */
 int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
                            const double *S, const int32_t *k_max, int32_t *k_star, double *W_star,
                            int32_t *m_at_star, dro_stream_t stream);

@@ -8,8 +8,7 @@ from .api import (Context, Problem, Groups, DroError, dro_validate, dro_cost_eva
                   dro_cost_eval_noalloc,
                   dro_argmin_reservation, dro_exact_table, dro_continuous_dual, class_quantile,
                   class_moments, dro_reservation_cost, dro_baseline_reservations, bcd_init_state,
-                  bcd_block_step,
-                  DRO_FLAG_BAND_FULL, DRO_FLAG_BAND_MARGIN)
+                  bcd_block_step)
 from ._native import LIB_PATH, NativeMissing, load as load_native
 
 __all__ = ["Context", "Problem", "Groups", "DroError", "dro_validate", "dro_cost_eval",
@@ -17,5 +16,5 @@ __all__ = ["Context", "Problem", "Groups", "DroError", "dro_validate", "dro_cost
            "dro_argmin_reservation", "dro_exact_table", "dro_continuous_dual", "class_quantile",
            "class_moments", "dro_reservation_cost", "dro_baseline_reservations", "bcd_init_state",
            "bcd_block_step",
-           "DRO_FLAG_BAND_FULL", "DRO_FLAG_BAND_MARGIN", "LIB_PATH", "NativeMissing",
+           "LIB_PATH", "NativeMissing",
            "load_native"]

@@ -43,7 +43,6 @@ EXPORTS = {
     "dro_destroy": (None, [P]),
     "dro_last_error": (ct.c_char_p, [P]),
     "dro_validate": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P]),
-    "dro_take_flags": (ct.c_int, [P, ct.POINTER(ct.c_uint32)]),
     "dro_cost_eval": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P]),
     "dro_cost_eval_noalloc": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P]),
     "dro_argmin_reservation": (ct.c_int, [P, ct.POINTER(ProblemStruct), i32, P, P, P, P, P, P, P]),

@@ -15,9 +15,6 @@ import torch
 
 from . import _native
 
-DRO_FLAG_BAND_FULL = 1
-DRO_FLAG_BAND_MARGIN = 2
-
 
 class DroError(RuntimeError):
     def __init__(self, code: int, where: str, detail: str):
@@ -84,11 +81,6 @@ class Context:
     def check(self, rc: int, where: str):
         if rc != 0:
             raise DroError(rc, where, f"{self._lib.dro_strerror(rc).decode()}: {self.last_error()}")
-
-    def take_flags(self) -> int:
-        v = ct.c_uint32(0)
-        self.check(self._lib.dro_take_flags(self._h, ct.byref(v)), "dro_take_flags")
-        return int(v.value)
 
 
 @dataclass

@@ -17,7 +17,6 @@ struct dro_ctx {
     int dense_bpc = 1;  // resident dense blocks per compute unit
     void *ws = nullptr;
     size_t ws_size = 0;
-    uint32_t *flags = nullptr;  // device word of DRO_FLAG_* bits
     void *scratch = nullptr;    // device address of this device's no-allocation scratch array
     char err[1024] = {0};
     // host staging of the configuration-space count table (kept alive until
@@ -324,126 +323,6 @@ QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
     return q;
 }
 
-// Scratch of the exact argmin: the screening band, the segments' prefix counts
-// and sums (from which the exact S of each candidate, and the exact table of
-// any (e, c) whose band did not settle its optimum, are formed), the value
-// histogram they come from unless the caller has one, and the [E*C][K] table.
-struct RefineBufs {
-    int32_t *cand, *count;
-    double *thresh, *chunk_min;
-    int32_t *need;
-    uint32_t *any;
-    QuantBufs qb;
-    uint32_t *cnt;
-    uint64_t *sum;
-    double *Wt;
-    int32_t *mt;
-};
-
-size_t band_chunks(int K) { return (size_t)(K + kBandKC - 1) / kBandKC; }
-
-size_t refine_bytes(const dro_problem *p, int EC, int num_cu, bool with_hist)
-{
-    const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
-    return rup((size_t)EC * kBandCap * 4) + rup((size_t)EC * 4) + rup((size_t)EC * 8) +
-           rup((size_t)EC * band_chunks(p->K) * 8) + rup((size_t)EC * 4) + rup(4) +
-           (with_hist ? quantile_bytes(p, num_cu) : 0) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8) +
-           rup(eck * 8) + rup(eck * 4);
-}
-
-RefineBufs take_refine(Arena &ar, const dro_problem *p, int EC, int num_cu, bool with_hist)
-{
-    RefineBufs r;
-    const size_t bins = (size_t)p->S * kHistBins, eck = (size_t)EC * p->K;
-    r.cand = ar.take<int32_t>((size_t)EC * kBandCap);
-    r.count = ar.take<int32_t>(EC);
-    r.thresh = ar.take<double>(EC);
-    r.chunk_min = ar.take<double>((size_t)EC * band_chunks(p->K));
-    r.need = ar.take<int32_t>(EC);
-    r.any = ar.take<uint32_t>(1);
-    r.qb = with_hist ? take_quantile(ar, p, num_cu) : QuantBufs{nullptr, nullptr, 0};
-    r.cnt = ar.take<uint32_t>(bins);
-    r.sum = ar.take<uint64_t>(prefix_sum_words(p->S));
-    r.Wt = ar.take<double>(eck);
-    r.mt = ar.take<int32_t>(eck);
-    return r;
-}
-
-// Value histogram (into rb.qb) and prefix counts and sums of every segment.
-int run_prefix(dro_ctx *ctx, const dro_problem *p, const RefineBufs &rb, hipStream_t st)
-{
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, rb.qb.B, rb.qb.part, rb.qb.hist, st));
-    HIPCHK(launch_prefix(rb.qb.hist, p->S, rb.cnt, rb.sum, st));
-    return DRO_OK;
-}
-
-// Screen and finalize for all (e, c) (c_only < 0) or for one class, over the
-// prefix counts and sums already in rb.cnt, rb.sum.
-int run_argmin(dro_ctx *ctx, const dro_problem *p, int E, const float *eps, const double *S,
-               const int32_t *k_max, int e_row, int c_only, const RefineBufs &rb,
-               int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
-{
-    const int EC = E * p->C;
-    HIPCHK(launch_fill_u32(reinterpret_cast<uint32_t *>(rb.need), EC, 0u, st));
-    HIPCHK(launch_fill_u32(rb.any, 1, 0u, st));
-    BandArgs b{};
-    b.S = S;
-    b.offsets = p->offsets;
-    b.seg = p->seg;
-    b.L = p->L;
-    b.lam = p->lam;
-    b.c_p = p->c_p;
-    b.c_w = p->c_w;
-    b.eps = eps;
-    b.k_max = k_max;
-    b.E = E;
-    b.C = p->C;
-    b.K = p->K;
-    b.M = p->M;
-    b.e_row = e_row;
-    b.c_only = c_only;
-    b.cand = rb.cand;
-    b.count = rb.count;
-    b.thresh = rb.thresh;
-    b.flags = ctx->flags;
-    HIPCHK(launch_band(b, rb.chunk_min, st));
-
-    FinalArgs f{};
-    f.offsets = p->offsets;
-    f.seg = p->seg;
-    f.L = p->L;
-    f.eta = p->eta;
-    f.lam = p->lam;
-    f.c_p = p->c_p;
-    f.c_w = p->c_w;
-    f.eps = eps;
-    f.cnt = rb.cnt;
-    f.sum = rb.sum;
-    f.cand = rb.cand;
-    f.count = rb.count;
-    f.thresh = rb.thresh;
-    f.C = p->C;
-    f.M = p->M;
-    f.EC = EC;
-    f.e_row = e_row;
-    f.c_only = c_only;
-    f.k_star = k_star;
-    f.W_star = W_star;
-    f.m_at_star = m_at_star;
-    f.flags = ctx->flags;
-    f.need = rb.need;
-    f.any = rb.any;
-    HIPCHK(launch_finalize(f, st));
-
-    // Where the band did not settle the optimum (it overflowed, or the optimum sat
-    // near its edge), the exact table of that (e, c) decides.  The kernels do
-    // nothing unless some (e, c) needs it.
-    HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, k_max,
-                              nullptr, p->S, E, p->C, p->K, p->M, rb.cnt, rb.sum, rb.Wt, rb.mt,
-                              k_star, W_star, m_at_star, st, rb.need, rb.any, false));
-    return DRO_OK;
-}
-
 int run_quantile(dro_ctx *ctx, const dro_problem *p, const QuantBufs &qb, int32_t *q_value,
                  int64_t *q_rank, hipStream_t st)
 {
@@ -540,16 +419,6 @@ int dro_create(int hip_device, dro_ctx **out)
         (void)hipGetLastError();
         ctx->scratch = nullptr;
     }
-    if (hipMalloc(&ctx->flags, sizeof(uint32_t)) != hipSuccess) {
-        (void)hipGetLastError();
-        delete ctx;
-        return DRO_ENOMEM;
-    }
-    if (hipMemset(ctx->flags, 0, sizeof(uint32_t)) != hipSuccess) {
-        (void)hipFree(ctx->flags);
-        delete ctx;
-        return DRO_EHIP;
-    }
     *out = ctx;
     return DRO_OK;
 }
@@ -560,21 +429,10 @@ void dro_destroy(dro_ctx *ctx)
     DeviceGuard g(ctx->device);  // best effort: destroy returns nothing
     (void)hipDeviceSynchronize();
     if (ctx->ws) (void)hipFree(ctx->ws);
-    if (ctx->flags) (void)hipFree(ctx->flags);
     delete ctx;
 }
 
 const char *dro_last_error(const dro_ctx *ctx) { return ctx ? ctx->err : "no context"; }
-
-int dro_take_flags(dro_ctx *ctx, uint32_t *flags_out)
-{
-    if (!ctx || !flags_out) return fail(ctx, DRO_EINVAL, "NULL argument");
-    ENTER_DEVICE(ctx);
-    HIPCHK(hipDeviceSynchronize());
-    HIPCHK(hipMemcpy(flags_out, ctx->flags, sizeof(uint32_t), hipMemcpyDeviceToHost));
-    HIPCHK(hipMemset(ctx->flags, 0, sizeof(uint32_t)));
-    return DRO_OK;
-}
 
 int dro_validate(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
                  dro_stream_t stream)
@@ -711,18 +569,22 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     if ((rc = check_rows(ctx, E, p->C))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    const int EC = E * p->C;
-    rc = ensure_ws(ctx, stage_bytes(p) + refine_bytes(p, EC, ctx->num_cu, true), st);
+    const size_t eck = (size_t)E * p->C * p->K;
+    rc = ensure_ws(ctx, stage_bytes(p) + rup(eck * 8) + rup(eck * 4), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    RefineBufs rb = take_refine(ar, p, EC, ctx->num_cu, true);
-    rc = run_prefix(ctx, p, rb, st);
-    if (rc) return rc;
-    return run_argmin(ctx, p, E, eps, S, k_max, 0, -1, rb, k_star, W_star, m_at_star, st);
+    double *W = ar.take<double>(eck);
+    int32_t *m_star = ar.take<int32_t>(eck);
+    // S is exact, so W (the exact-spec J minimised over m) is too, and the
+    // lowest-index optimum is a plain minimum over k
+    HIPCHK(launch_min_over_lambda(S, p->offsets, p->seg, p->lam, eps, E, p->C, p->K, p->M, W, m_star,
+                                  st));
+    HIPCHK(launch_table_argmin(W, m_star, k_max, E, p->C, p->K, k_star, W_star, m_at_star, st));
+    return DRO_OK;
 }
 
 int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t *q_rank,
@@ -918,9 +780,10 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const int C = p->C;
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const size_t ckm = (size_t)C * p->K * p->M;
-    const size_t need = rup(ckm * 8) + quantile_bytes(p, ctx->num_cu) +
-                        refine_bytes(p, C, ctx->num_cu, false) + rup((size_t)C * 8) +
-                        3 * rup((size_t)C * 4);
+    const size_t bins = (size_t)p->S * kHistBins;
+    const size_t need = rup(ckm * 8) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) +
+                        rup(prefix_sum_words(p->S) * 8) + rup((size_t)C * p->K * 8) +
+                        rup((size_t)C * 8) + rup((size_t)C * 4);
     rc = ensure_ws(ctx, stage_bytes(p) + need, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
@@ -930,27 +793,24 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     p = &q;
     double *S = ar.take<double>(ckm);
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
-    RefineBufs rb = take_refine(ar, p, C, ctx->num_cu, false);
+    uint32_t *cnt = ar.take<uint32_t>(bins);
+    uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
+    double *W = ar.take<double>((size_t)C * p->K);
     int64_t *q_rank = ar.take<int64_t>(C);
-    int32_t *kmax = ar.take<int32_t>(C);
     int32_t *kcur = ar.take<int32_t>(C);
 
     rc = run_quantile(ctx, p, qb, out->q_value, q_rank, st);
     if (rc) return rc;
     // the quantile's value histogram also gives the prefix counts and sums of
-    // the dense epilogue and of the exact argmin
-    HIPCHK(launch_prefix(qb.hist, p->S, rb.cnt, rb.sum, st));
-    rc = run_dense(ctx, p, S, rb.cnt, rb.sum, pl, st);
+    // the dense epilogue
+    HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
+    rc = run_dense(ctx, p, S, cnt, sum, pl, st);
     if (rc) return rc;
+    HIPCHK(launch_min_over_lambda(S, p->offsets, p->seg, p->lam, eps, 1, C, p->K, p->M, W, nullptr,
+                                  st));
     HIPCHK(hipMemcpyAsync(kcur, k_prev, sizeof(int32_t) * C, hipMemcpyDeviceToDevice, st));
-    for (int c = 0; c < C; ++c) {
-        HIPCHK(launch_bcd_kmax(p->eta, C, p->K, grp->G, grp->cap, grp->conc, grp->kappa, kcur, c,
-                               kmax, out->feasible, st));
-        rc = run_argmin(ctx, p, 1, eps, S, kmax, 0, c, rb, kcur, out->W_star, nullptr, st);
-        if (rc) return rc;
-    }
-    HIPCHK(launch_bcd_finish(p->eta, C, p->K, grp->G, grp->conc, grp->kappa, kcur, out->usage,
-                             out->k_next, st));
+    HIPCHK(launch_bcd_sweep(W, p->eta, C, p->K, grp->G, grp->cap, grp->conc, grp->kappa, kcur,
+                            out->k_next, out->W_star, out->feasible, out->usage, st));
     return DRO_OK;
 }
 

@@ -70,59 +70,6 @@ hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const
                                   const float *lam, const float *eps, int E, int C, int K, int M,
                                   double *W, int32_t *m_star, hipStream_t st);
 
-// ---- exact screening / refine ----------------------------------------------
-constexpr int kBandCap = 256;     // candidates kept per (e, c)
-constexpr double kBandTau = 1e-4; // relative width of the screening band
-constexpr int kBandKC = 16;       // grid points per screening block
-
-struct BandArgs {
-    const double *S;  // approximate [C][K][M]
-    const int64_t *offsets;
-    const int32_t *seg;
-    const int32_t *L;
-    const float *lam;
-    const float *c_p;
-    const float *c_w;
-    const float *eps;     // [E][C]
-    const int32_t *k_max; // [C] or null
-    int E, C, K, M;
-    int e_row, c_only;    // c_only >= 0: one (e_row, c_only) problem only
-    int32_t *cand;        // [EC][kBandCap] packed k * M + m
-    int32_t *count;       // [EC] (raw count; may exceed kBandCap)
-    double *thresh;       // [EC]
-    uint32_t *flags;
-};
-// chunk_min: [EC][ceil(K / kBandKC)] scratch
-hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st);
-
-// Exact S of each screened candidate from the prefix counts and sums of its
-// class's segment (cnt, sum: [S][kHistBins], from launch_prefix), its exact J,
-// and the lowest-index optimum of every (e, c).
-struct FinalArgs {
-    const int64_t *offsets;
-    const int32_t *seg;
-    const int32_t *L;
-    const int32_t *eta;
-    const float *lam;
-    const float *c_p;
-    const float *c_w;
-    const float *eps;
-    const uint32_t *cnt;
-    const uint64_t *sum;
-    const int32_t *cand;
-    const int32_t *count;
-    const double *thresh;
-    int C, M, EC;
-    int e_row, c_only;
-    int32_t *k_star;
-    double *W_star;
-    int32_t *m_at_star;
-    uint32_t *flags;
-    int32_t *need;   // [EC] 1 where the band did not settle the optimum (may be null)
-    uint32_t *any;   // set to 1 when some need[ec] is 1
-};
-hipError_t launch_finalize(const FinalArgs &a, hipStream_t st);
-
 // ---- quantile ----------------------------------------------------------------
 constexpr int kHistBins = 32769;   // values 0 .. 2^15
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st);
@@ -131,10 +78,8 @@ hipError_t hist_prepare();
 // blocks per segment for the histogram pass
 int hist_parts(int S, long long max_seg, int num_cu);
 // hist: [S][kHistBins]; part: [S][B][kHistBins] scratch (unused when B == 1).
-// With a gate, the kernels do nothing while *gate is 0.
 hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
-                            uint32_t *part, uint32_t *hist, hipStream_t st,
-                            const uint32_t *gate = nullptr);
+                            uint32_t *part, uint32_t *hist, hipStream_t st);
 hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st);
@@ -150,21 +95,20 @@ inline size_t prefix_sum_words(int S)
     return (size_t)S * kHistBins + (size_t)S * kPrefixChunks * 2;
 }
 // cnt[s][v] = #{x <= v}, sum[s][v] = sum of the samples <= v of segment s, from
-// its value histogram; with a gate, nothing runs while *gate is 0.
-hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
-                         const uint32_t *gate = nullptr);
+// its value histogram.
+hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st);
 // cnt: [S][kHistBins] u32, sum: prefix_sum_words(S) u64 scratch; k_star == null skips the argmin.
-// With need ([E*C]), only the rows with need[e*C + c] != 0 are computed and only
-// their k_star, W_star, m_at_star written; with a gate, nothing runs while *gate is 0.
-// with_prefix = false takes cnt and sum as already formed from hist.
 hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const int32_t *L,
                               const int32_t *eta, const float *lam, const float *c_p,
                               const float *c_w, const float *eps, const int32_t *k_max,
                               const uint32_t *hist, int S, int E, int C, int K, int M,
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
-                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st,
-                              const int32_t *need = nullptr, const uint32_t *gate = nullptr,
-                              bool with_prefix = true);
+                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st);
+// Per (e, c): the lowest k <= k_max[c] (k_max may be null: K - 1) with the
+// smallest W[e,c,k], W there, and m_star there (m_at_star may be null).
+hipError_t launch_table_argmin(const double *W, const int32_t *m_star, const int32_t *k_max,
+                               int E, int C, int K, int32_t *k_star, double *W_star,
+                               int32_t *m_at_star, hipStream_t st);
 
 // continuous-multiplier dual over the same prefix counts (gamma: the smallest minimiser)
 hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, const int32_t *L,
@@ -196,12 +140,12 @@ hipError_t launch_baselines(int C, const int64_t *count, const int64_t *sum, con
 hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
                            const int32_t *eta, int C, int K, long long max_n,
                            unsigned long long *sums, int32_t *k0, hipStream_t st);
-hipError_t launch_bcd_kmax(const int32_t *eta, int C, int K, int G, const float *cap,
-                           const float *conc, float kappa, const int32_t *kcur, int c,
-                           int32_t *kmax, uint8_t *feasible, hipStream_t st);
-hipError_t launch_bcd_finish(const int32_t *eta, int C, int K, int G, const float *conc,
-                             float kappa, const int32_t *kcur, double *usage, int32_t *k_next,
-                             hipStream_t st);
+// The block step's Gauss-Seidel sweep over the exact W [C][K] (one radius row),
+// kcur [C] the state entering it (updated in place).
+hipError_t launch_bcd_sweep(const double *W, const int32_t *eta, int C, int K, int G,
+                            const float *cap, const float *conc, float kappa, int32_t *kcur,
+                            int32_t *k_next, double *W_star, uint8_t *feasible, double *usage,
+                            hipStream_t st);
 
 // ---- serving model: routing LP, prefix caching, configuration search -------------
 struct SvcArgs {

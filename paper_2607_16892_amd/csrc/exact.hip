@@ -1,4 +1,5 @@
-// Exact parts of the reservation path: the screened argmin refine, the
+// Exact parts of the reservation path: the value histograms and prefix sums,
+// the exact table (F1) and the argmin over an exact W table, the
 // critical-fractile quantile, the block-step sweep and device-data checks.
 //
 // Compiled with -ffp-contract=off: every double expression below is the
@@ -75,271 +76,6 @@ __global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
     if (i < n) p[i] = v;
 }
 
-// ------------------------------------------------------------------ band ----
-// Screening.  A block takes one class c, up to kBandE radius rows e of it and
-// one chunk of kBandKC grid points, and reads each S[c, k, m] of the chunk once
-// for all of its rows:
-//   band_min:     per row, the smallest approximate dual value J~ = lam eps + S~ / N
-//                 of the chunk's pairs (k <= kmax, m <= m_first);
-//   band_collect: per row, the threshold T = (1 + tau) min J~ + slack from the
-//                 chunk minima, then every pair with J~ <= T appended to the row's
-//                 list through a global counter.  The list order is irrelevant: the
-//                 finalize evaluates every listed pair exactly and keeps the lowest
-//                 (J, k, m).
-// For lam_m >= max(c_p, c_w) every sample keeps its own point, so S is the SAA
-// sum for all such m and J can only grow with m: only the first of them
-// (m_first) can be a lowest-index minimiser, and the others are not screened.
-constexpr int kBandE = 8;  // radius rows per block (one when the call has a single row)
-
-template <int R>
-struct BandGroup {
-    int c, e0, ne, kmax, mlim;
-    double ninv, slack;
-    double ev[R];
-};
-
-template <int R>
-__device__ BandGroup<R> band_group(const BandArgs &a)
-{
-    __shared__ int s_mf;
-    BandGroup<R> q;
-    if (a.c_only >= 0) {
-        q.c = a.c_only;
-        q.e0 = a.e_row;
-        q.ne = 1;
-    } else {
-        q.c = (int)(blockIdx.x % a.C);
-        q.e0 = (int)(blockIdx.x / a.C) * R;
-        q.ne = min(R, a.E - q.e0);
-    }
-    const float cp = a.c_p[q.c], cw = a.c_w[q.c];
-    const float top = cp > cw ? cp : cw;
-    if (threadIdx.x == 0) s_mf = a.M - 1;
-    __syncthreads();
-    for (int m = threadIdx.x; m < a.M; m += blockDim.x)
-        if (a.lam[m] >= top) atomicMin(&s_mf, m);
-    __syncthreads();
-    q.mlim = s_mf;
-    q.kmax = a.K - 1;
-    if (a.k_max) {
-        const int km = a.k_max[q.c];
-        q.kmax = km < 0 ? 0 : (km > a.K - 1 ? a.K - 1 : km);
-    }
-    const int s = seg_of_x(a.seg, q.c);
-    q.ninv = 1.0 / (double)(a.offsets[s + 1] - a.offsets[s]);
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-        q.ev[r] = r < q.ne ? (double)a.eps[(long long)(q.e0 + r) * a.C + q.c] : 0.0;
-    q.slack = 1e-12 * (double)(cp + cw) * (double)a.L[q.c];
-    return q;
-}
-
-// Minimum over the 256-thread block of each of v[0..n): shuffles inside each
-// wave, then the four wave results through LDS.  Every thread gets them.
-template <int R>
-__device__ void block_min_rows(double (&v)[R], int n)
-{
-    __shared__ double sm[4][R];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        if (r >= n) break;
-        double x = v[r];
-        for (int d = 32; d > 0; d >>= 1) {
-            const double o = __shfl_xor(x, d, 64);
-            x = o < x ? o : x;
-        }
-        if (lane == 0) sm[wave][r] = x;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        if (r >= n) break;
-        double x = sm[0][r];
-        for (int w = 1; w < 4; ++w) x = sm[w][r] < x ? sm[w][r] : x;
-        v[r] = x;
-    }
-    __syncthreads();
-}
-
-template <int R>
-__global__ __launch_bounds__(256) void band_min_kernel(BandArgs a, double *chunk_min, int nchunks)
-{
-    const BandGroup<R> q = band_group<R>(a);
-    const int k0 = blockIdx.y * kBandKC;
-    const int k1 = min(k0 + kBandKC - 1, q.kmax);
-    const int nm = q.mlim + 1;
-    const int npair = k1 >= k0 ? (k1 - k0 + 1) * nm : 0;
-    double lmin[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) lmin[r] = __builtin_inf();
-    for (int i = threadIdx.x; i < npair; i += 256) {
-        const int k = k0 + i / nm, m = i % nm;
-        const double sn = a.S[((long long)q.c * a.K + k) * a.M + m] * q.ninv;
-        const double lm = (double)a.lam[m];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            if (r >= q.ne) break;
-            const double J = lm * q.ev[r] + sn;
-            lmin[r] = J < lmin[r] ? J : lmin[r];
-        }
-    }
-    block_min_rows<R>(lmin, q.ne);
-    if (threadIdx.x < q.ne) {
-        const int ec = (q.e0 + threadIdx.x) * a.C + q.c;
-        double r = lmin[0];
-#pragma unroll
-        for (int i = 1; i < R; ++i)
-            if (i == (int)threadIdx.x) r = lmin[i];
-        chunk_min[(long long)ec * nchunks + blockIdx.y] = r;
-    }
-}
-
-template <int R>
-__global__ __launch_bounds__(256) void band_collect_kernel(BandArgs a, const double *chunk_min,
-                                                           int nchunks)
-{
-    const BandGroup<R> q = band_group<R>(a);
-    double T[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        T[r] = __builtin_inf();
-        if (r < q.ne) {
-            const int ec = (q.e0 + r) * a.C + q.c;
-            for (int i = threadIdx.x; i < nchunks; i += 256) {
-                const double v = chunk_min[(long long)ec * nchunks + i];
-                T[r] = v < T[r] ? v : T[r];
-            }
-        }
-    }
-    block_min_rows<R>(T, q.ne);
-#pragma unroll
-    for (int r = 0; r < R; ++r) T[r] = T[r] + kBandTau * T[r] + q.slack;
-    const int k0 = blockIdx.y * kBandKC;
-    const int k1 = min(k0 + kBandKC - 1, q.kmax);
-    const int nm = q.mlim + 1;
-    const int npair = k1 >= k0 ? (k1 - k0 + 1) * nm : 0;
-    for (int i = threadIdx.x; i < npair; i += 256) {
-        const int k = k0 + i / nm, m = i % nm;
-        const double sn = a.S[((long long)q.c * a.K + k) * a.M + m] * q.ninv;
-        const double lm = (double)a.lam[m];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            if (r >= q.ne) break;
-            if (lm * q.ev[r] + sn <= T[r]) {
-                const int ec = (q.e0 + r) * a.C + q.c;
-                const int slot = atomicAdd(&a.count[ec], 1);
-                if (slot < kBandCap) a.cand[(long long)ec * kBandCap + slot] = k * a.M + m;
-            }
-        }
-    }
-    if (blockIdx.y == 0 && threadIdx.x < q.ne) {
-        double t = T[0];
-#pragma unroll
-        for (int i = 1; i < R; ++i)
-            if (i == (int)threadIdx.x) t = T[i];
-        a.thresh[(q.e0 + threadIdx.x) * a.C + q.c] = t;
-    }
-}
-
-hipError_t launch_band(const BandArgs &a, double *chunk_min, hipStream_t st)
-{
-    const int nchunks = (a.K + kBandKC - 1) / kBandKC;
-    const int EC = a.c_only >= 0 ? 1 : a.E * a.C;
-    int32_t *count = a.count + (a.c_only >= 0 ? (a.e_row * a.C + a.c_only) : 0);
-    hipLaunchKernelGGL(fill_u32_kernel, dim3((EC + 255) / 256), dim3(256), 0, st,
-                       reinterpret_cast<uint32_t *>(count), (long long)EC, 0u);
-    if (a.c_only >= 0 || a.E == 1) {
-        const int groups = a.c_only >= 0 ? 1 : a.C;
-        hipLaunchKernelGGL(band_min_kernel<1>, dim3(groups, nchunks), dim3(256), 0, st, a,
-                           chunk_min, nchunks);
-        hipLaunchKernelGGL(band_collect_kernel<1>, dim3(groups, nchunks), dim3(256), 0, st, a,
-                           (const double *)chunk_min, nchunks);
-    } else {
-        const int groups = a.C * ((a.E + kBandE - 1) / kBandE);
-        hipLaunchKernelGGL(band_min_kernel<kBandE>, dim3(groups, nchunks), dim3(256), 0, st, a,
-                           chunk_min, nchunks);
-        hipLaunchKernelGGL(band_collect_kernel<kBandE>, dim3(groups, nchunks), dim3(256), 0, st, a,
-                           (const double *)chunk_min, nchunks);
-    }
-    return hipGetLastError();
-}
-
-// -------------------------------------------------------------- finalize ----
-// Block per ec: the exact S of every screened candidate from the segment's
-// prefix counts and sums, its exact J, then the lowest (k, m) with the
-// smallest J (candidates are packed k * M + m, so one integer orders them).
-__global__ __launch_bounds__(256) void finalize_kernel(FinalArgs a)
-{
-    const int ec = (a.c_only >= 0) ? (a.e_row * a.C + a.c_only) : (int)blockIdx.x;
-    const int e = ec / a.C, c = ec % a.C;
-    const int t = threadIdx.x;
-    const int s = seg_of_x(a.seg, c);
-    const int64_t Ni = a.offsets[s + 1] - a.offsets[s];
-    const double N = (double)Ni;
-    const double ev = (double)a.eps[(long long)e * a.C + c];
-    const int64_t L = a.L[c];
-    const int64_t CP = fix33(a.c_p[c]), CW = fix33(a.c_w[c]);
-    const uint32_t *cn = a.cnt + (long long)s * kHistBins;
-    const uint64_t *sm = a.sum + (long long)s * kHistBins;
-    const int raw = a.count[ec];
-    const int cnt = min(raw, kBandCap);
-
-    double bJ = __builtin_inf();
-    int bkey = 0x7fffffff;
-    for (int i = t; i < cnt; i += 256) {
-        const int key = a.cand[(long long)ec * kBandCap + i];
-        const int k = key / a.M, m = key % a.M;
-        const unsigned __int128 S = exact_S_prefix(cn, sm, Ni, L, a.eta[k], CP, CW, fix33(a.lam[m]));
-        const double J = __dadd_rn(__dmul_rn((double)a.lam[m], ev),
-                                   __ddiv_rn(fix128_to_double((uint64_t)S, (uint64_t)(S >> 64)), N));
-        if (J < bJ || (J == bJ && key < bkey)) {
-            bJ = J;
-            bkey = key;
-        }
-    }
-    __shared__ double sJ[256];
-    __shared__ int sK[256];
-    sJ[t] = bJ;
-    sK[t] = bkey;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (t < w) {
-            const double j2 = sJ[t + w];
-            const int k2 = sK[t + w];
-            if (j2 < sJ[t] || (j2 == sJ[t] && k2 < sK[t])) {
-                sJ[t] = j2;
-                sK[t] = k2;
-            }
-        }
-        __syncthreads();
-    }
-    if (t == 0) {
-        const int key = sK[0];
-        a.k_star[ec] = key / a.M;
-        a.W_star[ec] = sJ[0];
-        if (a.m_at_star) a.m_at_star[ec] = key % a.M;
-        // the exact optimum must sit well inside the screening band, and the band
-        // must have fitted; otherwise the exact table of this (e, c) decides
-        const double T = a.thresh[ec];
-        const bool margin = !(sJ[0] * (1.0 + 0.5 * kBandTau) < T) || cnt == 0;
-        const bool full = raw > kBandCap;
-        if (margin) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_MARGIN);
-        if (full) atomicOr(a.flags, (uint32_t)DRO_FLAG_BAND_FULL);
-        if (a.need) {
-            a.need[ec] = (margin || full) ? 1 : 0;
-            if (margin || full) atomicOr(a.any, 1u);
-        }
-    }
-}
-
-hipError_t launch_finalize(const FinalArgs &a, hipStream_t st)
-{
-    const int blocks = a.c_only >= 0 ? 1 : a.EC;
-    hipLaunchKernelGGL(finalize_kernel, dim3(blocks), dim3(256), 0, st, a);
-    return hipGetLastError();
-}
-
 // -------------------------------------------------------------- quantile ----
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 {
@@ -358,11 +94,9 @@ constexpr int kHistThreads = 1024;
 
 __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *offsets,
                                                                  const int32_t *xi, int B,
-                                                                 uint32_t *part,
-                                                                 const uint32_t *gate)
+                                                                 uint32_t *part)
 {
     extern __shared__ uint32_t h[];  // kHistBins words
-    if (gate && *gate == 0u) return;
     const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
     const long long n0 = offsets[s], N = offsets[s + 1] - n0;
     const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
@@ -403,10 +137,8 @@ __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *
 }
 
 // hist[s][v] = sum over b of part[s][b][v]
-__global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t *hist,
-                                   const uint32_t *gate)
+__global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t *hist)
 {
-    if (gate && *gate == 0u) return;
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (long long)S * kHistBins) return;
     const long long s = i / kHistBins, v = i % kHistBins;
@@ -435,16 +167,16 @@ int hist_parts(int S, long long max_seg, int num_cu)
 }
 
 hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
-                            uint32_t *part, uint32_t *hist, hipStream_t st, const uint32_t *gate)
+                            uint32_t *part, uint32_t *hist, hipStream_t st)
 {
     if (S <= 0) return hipSuccess;
     uint32_t *dst = B == 1 ? hist : part;
     hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((long long)S * B)), dim3(kHistThreads),
-                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, dst, gate);
+                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, dst);
     if (B > 1) {
         const long long n = (long long)S * kHistBins;
         hipLaunchKernelGGL(hist_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                           (const uint32_t *)part, S, B, hist, gate);
+                           (const uint32_t *)part, S, B, hist);
     }
     return hipGetLastError();
 }
@@ -592,71 +324,104 @@ hipError_t launch_bcd_init(const int64_t *offsets, const int32_t *seg, const int
 }
 
 // Capacity bound of class c (the memory-capacity constraint of Sec. 3.4), then the largest admissible k.
-__global__ void bcd_kmax_kernel(const int32_t *eta, int C, int K, int G, const float *cap,
-                                const float *conc, float kappa, const int32_t *kcur, int c,
-                                int32_t *kmax, uint8_t *feasible)
-{
-    if (threadIdx.x != 0) return;
-    const double onek = __dadd_rn(1.0, (double)kappa);
-    double bound = __builtin_inf();
-    for (int g = 0; g < G; ++g) {
-        const double u = (double)conc[c * G + g];
-        if (!(u > 0.0)) continue;
-        double sum = 0.0;
-        for (int c2 = 0; c2 < C; ++c2) {
-            if (c2 == c) continue;
-            sum = __dadd_rn(sum, __dmul_rn((double)conc[c2 * G + g], (double)eta[clampk(kcur[c2], K)]));
-        }
-        const double other = __dmul_rn(onek, sum);
-        const double num = __dsub_rn((double)cap[g], other);
-        const double den = __dmul_rn(onek, u);
-        const double b = __ddiv_rn(num, den);
-        bound = b < bound ? b : bound;
-    }
-    // eta ascending: the largest k with eta[k] <= bound, or none
-    int km = -1, lo = 0, hi = K - 1;
-    while (lo <= hi) {
-        const int mid = (lo + hi) / 2;
-        if ((double)eta[mid] <= bound) {
-            km = mid;
-            lo = mid + 1;
-        } else {
-            hi = mid - 1;
-        }
-    }
-    feasible[c] = km >= 0 ? 1 : 0;
-    kmax[c] = km >= 0 ? km : 0;
-}
+// The Gauss-Seidel sweep of the block step, one workgroup: for c = 0..C-1 in
+// order, thread 0 forms the capacity bound of class c from the other classes'
+// current grid points (fp64, no contraction, ascending class order), then the
+// block takes the lowest argmin of the exact W[c, 0..kmax_c] (lowest k on
+// equal values), which updates k[c] before the next class.  kcur[C] holds the
+// state entering the sweep and is updated in place.
+constexpr int kSweepThreads = 1024;
 
-hipError_t launch_bcd_kmax(const int32_t *eta, int C, int K, int G, const float *cap,
-                           const float *conc, float kappa, const int32_t *kcur, int c,
-                           int32_t *kmax, uint8_t *feasible, hipStream_t st)
+__global__ __launch_bounds__(kSweepThreads) void bcd_sweep_kernel(
+    const double *W, const int32_t *eta, int C, int K, int G, const float *cap, const float *conc,
+    float kappa, int32_t *kcur, int32_t *k_next, double *W_star, uint8_t *feasible,
+    double *usage)
 {
-    hipLaunchKernelGGL(bcd_kmax_kernel, dim3(1), dim3(64), 0, st, eta, C, K, G, cap, conc, kappa,
-                       kcur, c, kmax, feasible);
-    return hipGetLastError();
-}
-
-__global__ void bcd_finish_kernel(const int32_t *eta, int C, int K, int G, const float *conc,
-                                  float kappa, const int32_t *kcur, double *usage, int32_t *k_next)
-{
-    const int t = threadIdx.x;
+    __shared__ int s_kmax;
+    __shared__ double sw[kSweepThreads / 64];
+    __shared__ int sk[kSweepThreads / 64];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const double onek = __dadd_rn(1.0, (double)kappa);
-    for (int g = t; g < G; g += blockDim.x) {
+    for (int c = 0; c < C; ++c) {
+        if (t == 0) {
+            double bound = __builtin_inf();
+            for (int g = 0; g < G; ++g) {
+                const double u = (double)conc[c * G + g];
+                if (!(u > 0.0)) continue;
+                double sum = 0.0;
+                for (int c2 = 0; c2 < C; ++c2) {
+                    if (c2 == c) continue;
+                    sum = __dadd_rn(sum, __dmul_rn((double)conc[c2 * G + g],
+                                                   (double)eta[clampk(kcur[c2], K)]));
+                }
+                const double other = __dmul_rn(onek, sum);
+                const double b = __ddiv_rn(__dsub_rn((double)cap[g], other), __dmul_rn(onek, u));
+                bound = b < bound ? b : bound;
+            }
+            // eta ascending: the largest k with eta[k] <= bound, or none
+            int km = -1, lo = 0, hi = K - 1;
+            while (lo <= hi) {
+                const int mid = (lo + hi) / 2;
+                if ((double)eta[mid] <= bound) {
+                    km = mid;
+                    lo = mid + 1;
+                } else {
+                    hi = mid - 1;
+                }
+            }
+            feasible[c] = km >= 0 ? 1 : 0;
+            s_kmax = km >= 0 ? km : 0;
+        }
+        __syncthreads();
+        const int kmax = s_kmax;
+        const double *w = W + (long long)c * K;
+        double bw = __builtin_inf();
+        int bk = 0x7fffffff;
+        for (int k = t; k <= kmax; k += kSweepThreads)
+            if (w[k] < bw) {  // k ascending per thread: its first minimiser
+                bw = w[k];
+                bk = k;
+            }
+        for (int d = 32; d > 0; d >>= 1) {
+            const double w2 = __shfl_xor(bw, d, 64);
+            const int k2 = __shfl_xor(bk, d, 64);
+            if (w2 < bw || (w2 == bw && k2 < bk)) {
+                bw = w2;
+                bk = k2;
+            }
+        }
+        if (lane == 0) {
+            sw[wave] = bw;
+            sk[wave] = bk;
+        }
+        __syncthreads();
+        if (t == 0) {
+            for (int i = 1; i < kSweepThreads / 64; ++i)
+                if (sw[i] < bw || (sw[i] == bw && sk[i] < bk)) {
+                    bw = sw[i];
+                    bk = sk[i];
+                }
+            kcur[c] = bk;
+            W_star[c] = bw;
+        }
+        __syncthreads();
+    }
+    for (int g = t; g < G; g += kSweepThreads) {
         double sum = 0.0;
         for (int c = 0; c < C; ++c)
             sum = __dadd_rn(sum, __dmul_rn((double)conc[c * G + g], (double)eta[clampk(kcur[c], K)]));
         usage[g] = __dmul_rn(onek, sum);
     }
-    for (int c = t; c < C; c += blockDim.x) k_next[c] = clampk(kcur[c], K);
+    for (int c = t; c < C; c += kSweepThreads) k_next[c] = clampk(kcur[c], K);
 }
 
-hipError_t launch_bcd_finish(const int32_t *eta, int C, int K, int G, const float *conc,
-                             float kappa, const int32_t *kcur, double *usage, int32_t *k_next,
-                             hipStream_t st)
+hipError_t launch_bcd_sweep(const double *W, const int32_t *eta, int C, int K, int G,
+                            const float *cap, const float *conc, float kappa, int32_t *kcur,
+                            int32_t *k_next, double *W_star, uint8_t *feasible, double *usage,
+                            hipStream_t st)
 {
-    hipLaunchKernelGGL(bcd_finish_kernel, dim3(1), dim3(256), 0, st, eta, C, K, G, conc, kappa,
-                       kcur, usage, k_next);
+    hipLaunchKernelGGL(bcd_sweep_kernel, dim3(1), dim3(kSweepThreads), 0, st, W, eta, C, K, G, cap,
+                       conc, kappa, kcur, k_next, W_star, feasible, usage);
     return hipGetLastError();
 }
 
@@ -735,11 +500,9 @@ __device__ __forceinline__ int pad32(int j) { return j + (j >> 5); }
 // Per (segment, chunk): the count and the value-weighted sum of the chunk's
 // bins, tot[(s * kPrefixChunks + ch) * 2 + {0, 1}].
 __global__ __launch_bounds__(kPrefixThreads) void chunk_total_kernel(const uint32_t *hist,
-                                                                     uint64_t *tot,
-                                                                     const uint32_t *gate)
+                                                                     uint64_t *tot)
 {
     __shared__ uint64_t rc[kPrefixThreads], rs[kPrefixThreads];
-    if (gate && *gate == 0u) return;
     const int ch = (int)(blockIdx.x % kPrefixChunks), s = (int)(blockIdx.x / kPrefixChunks);
     const int t = threadIdx.x;
     const uint32_t *h = hist + (long long)s * kHistBins;
@@ -768,11 +531,10 @@ __global__ __launch_bounds__(kPrefixThreads) void chunk_total_kernel(const uint3
 
 __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *hist,
                                                                 const uint64_t *tot, uint32_t *cnt,
-                                                                uint64_t *sum, const uint32_t *gate)
+                                                                uint64_t *sum)
 {
     __shared__ uint32_t hc[kPrefixChunk + kPrefixChunk / 32];
     __shared__ uint64_t rc[kPrefixThreads / 64], rs[kPrefixThreads / 64];
-    if (gate && *gate == 0u) return;
     const int ch = (int)(blockIdx.x % kPrefixChunks), s = (int)(blockIdx.x / kPrefixChunks);
     const int t = threadIdx.x;
     const uint32_t *h = hist + (long long)s * kHistBins;
@@ -830,17 +592,16 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(const uint32_t *
     }
 }
 
-hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st,
-                         const uint32_t *gate)
+hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *sum, hipStream_t st)
 {
     // chunk totals first (after the prefix sums in the same array), then each
     // chunk's scan starts from the totals of the chunks before it
     const long long blocks = (long long)S * kPrefixChunks;
     uint64_t *tot = sum + (long long)S * kHistBins;
     hipLaunchKernelGGL(chunk_total_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st,
-                       hist, tot, gate);
+                       hist, tot);
     hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)blocks), dim3(kPrefixThreads), 0, st, hist,
-                       (const uint64_t *)tot, cnt, sum, gate);
+                       (const uint64_t *)tot, cnt, sum);
     return hipGetLastError();
 }
 
@@ -856,8 +617,7 @@ template <int TM>
 __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
     const float *lam, const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt,
-    const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star,
-    const int32_t *need, const uint32_t *gate)
+    const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star)
 {
     __shared__ double rv[8][kTableThreads];
     __shared__ int rm[8][kTableThreads];
@@ -866,12 +626,6 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     const int c = (int)(blockIdx.x / kgroups);
     const int t = threadIdx.x, ml = t % TM;
     const int k = (int)(blockIdx.x % kgroups) * KB + t / TM;
-    if (gate && *gate == 0u) return;
-    if (need) {  // only the classes some radius row of which needs the table
-        bool any = false;
-        for (int e = 0; e < E; ++e) any = any || need[(long long)e * C + c] != 0;
-        if (!any) return;
-    }
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
     const int64_t L = L_[c], eta = eta_[k < K ? k : K - 1];
@@ -939,16 +693,14 @@ __global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
     }
 }
 
-// Block per (e, c): lowest k <= kmax with the smallest W, and the values there.
+// Block per (e, c): lowest k <= kmax with the smallest W, and the values there
+// (the exact optimum over a W table whose entries are exact-spec values).
 __global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, const int32_t *m_star,
                                                            const int32_t *k_max, int C, int K,
                                                            int32_t *k_star, double *W_star,
-                                                           int32_t *m_at_star, const int32_t *need,
-                                                           const uint32_t *gate)
+                                                           int32_t *m_at_star)
 {
     const int ec = blockIdx.x, c = ec % C, t = threadIdx.x;
-    if (gate && *gate == 0u) return;
-    if (need && need[ec] == 0) return;
     int kmax = K - 1;
     if (k_max) {
         kmax = k_max[c];
@@ -985,15 +737,23 @@ __global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, cons
     }
 }
 
+hipError_t launch_table_argmin(const double *W, const int32_t *m_star, const int32_t *k_max,
+                               int E, int C, int K, int32_t *k_star, double *W_star,
+                               int32_t *m_at_star, hipStream_t st)
+{
+    hipLaunchKernelGGL(table_argmin_kernel, dim3((unsigned)((long long)E * C)), dim3(256), 0, st, W,
+                       m_star, k_max, C, K, k_star, W_star, m_at_star);
+    return hipGetLastError();
+}
+
 hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const int32_t *L,
                               const int32_t *eta, const float *lam, const float *c_p,
                               const float *c_w, const float *eps, const int32_t *k_max,
                               const uint32_t *hist, int S, int E, int C, int K, int M,
                               uint32_t *cnt, uint64_t *sum, double *W, int32_t *m_star,
-                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st,
-                              const int32_t *need, const uint32_t *gate, bool with_prefix)
+                              int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
 {
-    if (with_prefix) HIPRET(launch_prefix(hist, S, cnt, sum, st, gate));
+    HIPRET(launch_prefix(hist, S, cnt, sum, st));
     int TM = 1;  // threads per grid point
     while (TM < M && TM < kTableThreads) TM *= 2;
     const int KB = kTableThreads / TM;
@@ -1002,7 +762,7 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
     case tm:                                                                                      \
         hipLaunchKernelGGL(exact_table_kernel<tm>, dim3((unsigned)n), dim3(kTableThreads), 0, st, \
                            offsets, seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,       \
-                           (const uint64_t *)sum, E, C, K, M, W, m_star, need, gate);            \
+                           (const uint64_t *)sum, E, C, K, M, W, m_star);                        \
         break;
     switch (TM) {
         DRO_TABLE_CASE(1)
@@ -1016,10 +776,7 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
         DRO_TABLE_CASE(256)
     }
 #undef DRO_TABLE_CASE
-    if (k_star)
-        hipLaunchKernelGGL(table_argmin_kernel, dim3(E * C), dim3(256), 0, st, (const double *)W,
-                           (const int32_t *)m_star, k_max, C, K, k_star, W_star, m_at_star, need,
-                           gate);
+    if (k_star) HIPRET(launch_table_argmin(W, m_star, k_max, E, C, K, k_star, W_star, m_at_star, st));
     return hipGetLastError();
 }
 

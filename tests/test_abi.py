@@ -32,7 +32,7 @@ def test_header_declares_the_entry_points():
     names = _declared()
     for n in ("dro_cost_eval", "dro_argmin_reservation", "class_quantile", "bcd_block_step",
               "bcd_init_state", "dro_create", "dro_destroy", "dro_validate", "dro_strerror",
-              "dro_last_error", "dro_take_flags"):
+              "dro_last_error", "dro_cost_eval_noalloc"):
         assert n in names
 
 

@@ -46,7 +46,6 @@ def test_whole_tables_against_the_oracle(ctx, dev, name):
     a = dro.dro_argmin_reservation(ctx, prob, eps, r["S"])
     q = dro.class_quantile(ctx, prob)
     torch.cuda.synchronize()
-    assert ctx.take_flags() == 0
     g = {k: v.cpu().numpy() for d in (r, a, q) for k, v in d.items()}
     del r
 
