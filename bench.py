@@ -54,7 +54,7 @@ PAPER_FLOPS_PER_EVAL = 7                 # 2 multiply-adds (4), a 3-way max (2),
 # stripped, identified by the hash prefix) and are reported as null for any
 # other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "09cc6c53cbf30cdb",
+    "dense_code_sha256_16": "83599eb12e88a3ba",
     "workload": "mixture-16x1M",
     "valu_instr_per_eval": 0.50659,    # SQ_INSTS_VALU x 64 / evaluations
     "clock_ghz": 2.378,                # GRBM_GUI_ACTIVE / 8 XCDs / duration
@@ -80,9 +80,12 @@ def dense_code_hash() -> str:
     i = hdr.index("struct DensePlan")  # the dense section's constants come before its structs
     consts = [ln for ln in hdr[:i].splitlines() if "constexpr" in ln]
     api = code("api.hip")
-    i = api.index("constexpr long long kMinWaves")
+    plan_consts = [ln for ln in api.splitlines()
+                   if any(f"constexpr long long {k} " in ln for k in ("kMinWaves", "kMinSlice",
+                                                                      "kMaxSlices"))]
+    i = api.index("DensePlan plan_dense(")
     plan = api[i:api.index("return pl;", i)]
-    text = code("dense.hip") + "\n" + "\n".join(consts) + "\n" + plan
+    text = code("dense.hip") + "\n" + "\n".join(consts + plan_consts) + "\n" + plan
     return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
 
 

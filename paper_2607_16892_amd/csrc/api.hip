@@ -18,6 +18,15 @@ struct dro_ctx {
     void *ws = nullptr;
     size_t ws_size = 0;
     void *scratch = nullptr;    // device address of this device's no-allocation scratch array
+    // The host-validated offsets and segment map last staged on the device, and
+    // the stream they were staged on: a call whose host arrays and stream match
+    // uses the staged copy without uploading it again.
+    void *stage = nullptr;
+    size_t stage_size = 0;
+    bool staged = false;
+    hipStream_t staged_stream = nullptr;
+    std::vector<int64_t> staged_off;
+    std::vector<int32_t> staged_seg;
     char err[1024] = {0};
     // host staging of the configuration-space count table (kept alive until
     // the next configuration search on this context has been enqueued)
@@ -197,16 +206,58 @@ size_t stage_bytes(const dro_problem *p)
     return rup((size_t)(p->S + 1) * 8) + (p->seg_h ? rup((size_t)p->C * 4) : 0);
 }
 
+// The offsets (and segment map) every kernel indexes with: the host copies of
+// the call, uploaded to the device.  Calls on the workspace keep them in the
+// ctx's staging buffer and skip the upload when the host arrays and the stream
+// equal the last ones staged; the no-allocation path stages them into its
+// arena on every call (the static array is shared by every ctx of the device).
 int stage_problem(dro_ctx *ctx, const dro_problem *p, Arena &ar, hipStream_t st, dro_problem *q)
 {
     *q = *p;
-    int64_t *off = ar.take<int64_t>((size_t)p->S + 1);
-    HIPCHK(hipMemcpyAsync(off, p->offsets_h, (size_t)(p->S + 1) * 8, hipMemcpyHostToDevice, st));
-    q->offsets = off;
+    const size_t ob = (size_t)(p->S + 1) * 8, sb = p->seg_h ? (size_t)p->C * 4 : 0;
+    char *dst;
+    if (ar.base != (char *)ctx->ws) {
+        dst = ar.take<char>(stage_bytes(p));
+    } else {
+        const bool same =
+            ctx->staged && ctx->staged_stream == st && ctx->staged_off.size() == (size_t)p->S + 1 &&
+            std::equal(p->offsets_h, p->offsets_h + p->S + 1, ctx->staged_off.begin()) &&
+            (p->seg_h ? ctx->staged_seg.size() == (size_t)p->C &&
+                            std::equal(p->seg_h, p->seg_h + p->C, ctx->staged_seg.begin())
+                      : ctx->staged_seg.empty());
+        if (same) {
+            q->offsets = reinterpret_cast<int64_t *>(ctx->stage);
+            if (p->seg_h) q->seg = reinterpret_cast<int32_t *>((char *)ctx->stage + rup(ob));
+            return DRO_OK;
+        }
+        ctx->staged = false;
+        if (stage_bytes(p) > ctx->stage_size) {
+            HIPCHK(hipDeviceSynchronize());  // earlier work may still read the old copy
+            if (ctx->stage) HIPCHK(hipFree(ctx->stage));
+            ctx->stage = nullptr;
+            ctx->stage_size = 0;
+            const size_t sz = stage_bytes(p) + (1u << 12);
+            if (hipMalloc(&ctx->stage, sz) != hipSuccess) {
+                (void)hipGetLastError();
+                ctx->stage = nullptr;
+                return fail(ctx, DRO_ENOMEM, "staging allocation of %zu bytes failed", sz);
+            }
+            ctx->stage_size = sz;
+        }
+        dst = (char *)ctx->stage;
+    }
+    HIPCHK(hipMemcpyAsync(dst, p->offsets_h, ob, hipMemcpyHostToDevice, st));
+    q->offsets = reinterpret_cast<int64_t *>(dst);
     if (p->seg_h) {
-        int32_t *seg = ar.take<int32_t>((size_t)p->C);
-        HIPCHK(hipMemcpyAsync(seg, p->seg_h, (size_t)p->C * 4, hipMemcpyHostToDevice, st));
-        q->seg = seg;
+        HIPCHK(hipMemcpyAsync(dst + rup(ob), p->seg_h, sb, hipMemcpyHostToDevice, st));
+        q->seg = reinterpret_cast<int32_t *>(dst + rup(ob));
+    }
+    if (dst == (char *)ctx->stage) {
+        ctx->staged_off.assign(p->offsets_h, p->offsets_h + p->S + 1);
+        if (p->seg_h) ctx->staged_seg.assign(p->seg_h, p->seg_h + p->C);
+        else ctx->staged_seg.clear();
+        ctx->staged_stream = st;
+        ctx->staged = true;
     }
     return DRO_OK;
 }
@@ -295,38 +346,24 @@ long long max_segment(const dro_problem *p)
 }
 
 struct QuantBufs {
-    uint32_t *hist, *part;
-    int B;
+    uint32_t *hist;  // [S][kHistBins]
+    int B;           // histogram blocks per segment
 };
 
-size_t quantile_bytes(const dro_problem *p, int num_cu)
-{
-    const int B = hist_parts(p->S, max_segment(p), num_cu);
-    return rup((size_t)p->S * kHistBins * 4) + (B > 1 ? rup((size_t)p->S * B * kHistBins * 4) : 0);
-}
-
-QuantBufs take_quantile_parts(Arena &ar, const dro_problem *p, int B)
-{
-    QuantBufs q;
-    q.B = B;
-    q.hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
-    q.part = q.B > 1 ? ar.take<uint32_t>((size_t)p->S * q.B * kHistBins) : nullptr;
-    return q;
-}
+size_t quantile_bytes(const dro_problem *p) { return rup((size_t)p->S * kHistBins * 4); }
 
 QuantBufs take_quantile(Arena &ar, const dro_problem *p, int num_cu)
 {
     QuantBufs q;
     q.B = hist_parts(p->S, max_segment(p), num_cu);
     q.hist = ar.take<uint32_t>((size_t)p->S * kHistBins);
-    q.part = q.B > 1 ? ar.take<uint32_t>((size_t)p->S * q.B * kHistBins) : nullptr;
     return q;
 }
 
 int run_quantile(dro_ctx *ctx, const dro_problem *p, const QuantBufs &qb, int32_t *q_value,
                  int64_t *q_rank, hipStream_t st)
 {
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_select(p->offsets, p->seg, p->c_p, p->c_w, qb.hist, p->C, q_value, q_rank, st));
     return DRO_OK;
 }
@@ -342,12 +379,13 @@ int check_rows(dro_ctx *ctx, int E, int C)
 bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 bool in_limits(float v) { return v >= 0x1p-10f && v <= 0x1p7f; }
 
-// Scratch of one dense evaluation beyond S: the staged offsets and segment
-// map, the value histogram with B parts per segment, the prefix counts and sums.
-size_t cost_eval_scratch_bytes(const dro_problem *p, int B)
+// Scratch of one dense evaluation beyond S: the value histogram, the prefix
+// counts and sums (and, on the no-allocation path, the staged offsets and
+// segment map).
+size_t cost_eval_scratch_bytes(const dro_problem *p, bool with_stage)
 {
     const size_t bins = (size_t)p->S * kHistBins;
-    return stage_bytes(p) + rup(bins * 4) + (B > 1 ? rup(bins * B * 4) : 0) + rup(bins * 4) +
+    return (with_stage ? stage_bytes(p) : 0) + quantile_bytes(p) + rup(bins * 4) +
            rup(prefix_sum_words(p->S) * 8);
 }
 
@@ -355,7 +393,7 @@ size_t cost_eval_scratch_bytes(const dro_problem *p, int B)
 // current): value counts and sample sums of every segment, the exact S into
 // Sbuf, then the minimum over the multipliers.
 int run_cost_eval(dro_ctx *ctx, const dro_problem *p, const Shape &sh, int E, const float *eps,
-                  double *W, int32_t *m_star, double *Sbuf, Arena &ar, int B, hipStream_t st)
+                  double *W, int32_t *m_star, double *Sbuf, Arena &ar, hipStream_t st)
 {
     dro_problem q;
     int rc = stage_problem(ctx, p, ar, st, &q);
@@ -363,10 +401,10 @@ int run_cost_eval(dro_ctx *ctx, const dro_problem *p, const Shape &sh, int E, co
     p = &q;
     const DensePlan pl = plan_dense(p->C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const size_t bins = (size_t)p->S * kHistBins;
-    const QuantBufs qb = take_quantile_parts(ar, p, B);
+    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
     uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
     rc = run_dense(ctx, p, Sbuf, cnt, sum, pl, st);
     if (rc) return rc;
@@ -429,6 +467,7 @@ void dro_destroy(dro_ctx *ctx)
     DeviceGuard g(ctx->device);  // best effort: destroy returns nothing
     (void)hipDeviceSynchronize();
     if (ctx->ws) (void)hipFree(ctx->ws);
+    if (ctx->stage) (void)hipFree(ctx->stage);
     delete ctx;
 }
 
@@ -522,12 +561,11 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t ckm = (size_t)p->C * p->K * p->M;
-    const int B = hist_parts(p->S, max_segment(p), ctx->num_cu);
-    rc = ensure_ws(ctx, (S ? 0 : rup(ckm * 8)) + cost_eval_scratch_bytes(p, B), st);
+    rc = ensure_ws(ctx, (S ? 0 : rup(ckm * 8)) + cost_eval_scratch_bytes(p, false), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     double *Sbuf = S ? S : ar.take<double>(ckm);
-    return run_cost_eval(ctx, p, sh, E, eps, W, m_star, Sbuf, ar, B, st);
+    return run_cost_eval(ctx, p, sh, E, eps, W, m_star, Sbuf, ar, st);
 }
 
 int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
@@ -542,19 +580,14 @@ int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const f
     if (!ctx->scratch)
         return fail(ctx, DRO_EHIP, "the scratch array's device address is unknown on device %d",
                     ctx->device);
-    // as many histogram parts as the array leaves room for (at most the
-    // workspace path's), down to one
-    const size_t cap = DRO_NOALLOC_SCRATCH_BYTES;
-    const size_t need1 = cost_eval_scratch_bytes(p, 1);
-    if (need1 > cap)
+    const size_t need = cost_eval_scratch_bytes(p, true);
+    if (need > (size_t)DRO_NOALLOC_SCRATCH_BYTES)
         return fail(ctx, DRO_ELIMIT,
                     "the problem needs %zu bytes of scratch; the no-allocation array holds %zu",
-                    need1, cap);
-    int B = hist_parts(p->S, max_segment(p), ctx->num_cu);
-    while (B > 1 && cost_eval_scratch_bytes(p, B) > cap) --B;
+                    need, (size_t)DRO_NOALLOC_SCRATCH_BYTES);
     ENTER_DEVICE(ctx);
     Arena ar{(char *)ctx->scratch, 0};
-    return run_cost_eval(ctx, p, sh, E, eps, W, m_star, S, ar, B, (hipStream_t)stream);
+    return run_cost_eval(ctx, p, sh, E, eps, W, m_star, S, ar, (hipStream_t)stream);
 }
 
 int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,
@@ -570,7 +603,7 @@ int dro_argmin_reservation(dro_ctx *ctx, const dro_problem *p, int32_t E, const 
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t eck = (size_t)E * p->C * p->K;
-    rc = ensure_ws(ctx, stage_bytes(p) + rup(eck * 8) + rup(eck * 4), st);
+    rc = ensure_ws(ctx, rup(eck * 8) + rup(eck * 4), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -596,7 +629,7 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     if (!q_value || !q_rank) return fail(ctx, DRO_EINVAL, "q_value and q_rank must be non-NULL");
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu), st);
+    rc = ensure_ws(ctx, quantile_bytes(p), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -620,7 +653,7 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
+    rc = ensure_ws(ctx, quantile_bytes(p) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -630,7 +663,7 @@ int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
     uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, k_max,
                               qb.hist, p->S, E, p->C, p->K, p->M, cnt, sum, W, m_star, k_star,
                               W_star, m_at_star, st));
@@ -649,7 +682,7 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
+    rc = ensure_ws(ctx, quantile_bytes(p) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -659,7 +692,7 @@ int dro_continuous_dual(dro_ctx *ctx, const dro_problem *p, int32_t E, const flo
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
     uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_continuous_dual(p->offsets, p->seg, p->L, p->eta, p->c_p, p->c_w, eps, qb.hist,
                                   p->S, E, p->C, p->K, cnt, sum, W, gamma, st));
     return DRO_OK;
@@ -675,7 +708,7 @@ int class_moments(dro_ctx *ctx, const dro_problem *p, int64_t *count, int64_t *s
         return fail(ctx, DRO_EINVAL, "count, sum, sumsq and xmax must be non-NULL");
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu), st);
+    rc = ensure_ws(ctx, quantile_bytes(p), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -683,7 +716,7 @@ int class_moments(dro_ctx *ctx, const dro_problem *p, int64_t *count, int64_t *s
     if (rc) return rc;
     p = &q;
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_moments(p->seg, qb.hist, p->C, count, sum, sumsq, xmax, st));
     return DRO_OK;
 }
@@ -701,7 +734,7 @@ int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const in
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t bins = (size_t)p->S * kHistBins;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
+    rc = ensure_ws(ctx, quantile_bytes(p) + rup(bins * 4) + rup(prefix_sum_words(p->S) * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -711,7 +744,7 @@ int dro_reservation_cost(dro_ctx *ctx, const dro_problem *p, int32_t R, const in
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
     uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_reservation_cost(p->offsets, p->seg, p->c_p, p->c_w, qb.hist, p->S, p->C, R,
                                    eta_r, cnt, sum, cost, cover, st));
     return DRO_OK;
@@ -752,7 +785,7 @@ int bcd_init_state(dro_ctx *ctx, const dro_problem *p, int32_t *k0, dro_stream_t
     if (!k0) return fail(ctx, DRO_EINVAL, "k0 must be non-NULL");
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, stage_bytes(p) + rup((size_t)p->C * 8), st);
+    rc = ensure_ws(ctx, rup((size_t)p->C * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -781,10 +814,10 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const DensePlan pl = plan_dense(C, p->K, p->M, sh.max_n, ctx->num_cu, ctx->dense_bpc);
     const size_t ckm = (size_t)C * p->K * p->M;
     const size_t bins = (size_t)p->S * kHistBins;
-    const size_t need = rup(ckm * 8) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) +
+    const size_t need = rup(ckm * 8) + quantile_bytes(p) + rup(bins * 4) +
                         rup(prefix_sum_words(p->S) * 8) + rup((size_t)C * p->K * 8) +
                         rup((size_t)C * 8) + rup((size_t)C * 4);
-    rc = ensure_ws(ctx, stage_bytes(p) + need, st);
+    rc = ensure_ws(ctx, need, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -966,7 +999,7 @@ int bcd_service_times(dro_ctx *ctx, const dro_problem *p, const dro_service *svc
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
-    rc = ensure_ws(ctx, stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + 4 * rup((size_t)C * 8), st);
+    rc = ensure_ws(ctx, quantile_bytes(p) + 4 * rup((size_t)C * 8), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
@@ -976,7 +1009,7 @@ int bcd_service_times(dro_ctx *ctx, const dro_problem *p, const dro_service *svc
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     int64_t *cnt = ar.take<int64_t>(C), *sum = ar.take<int64_t>(C), *ssq = ar.take<int64_t>(C);
     int32_t *xmax = ar.take<int32_t>(C);
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_moments(p->seg, qb.hist, C, cnt, sum, ssq, xmax, st));
     HIPCHK(launch_service_times(svc_args(svc, C), cnt, sum, ssq, T, ET2, st));
     return DRO_OK;
@@ -1097,7 +1130,7 @@ int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dr
     if (nz < 0) return fail(ctx, DRO_EHIP, "stream synchronisation failed");
     if (nz > kMaxConfigs) return fail(ctx, DRO_ELIMIT, "%lld configurations exceed 2^32", nz);
     const size_t bins = (size_t)p->S * kHistBins;
-    const size_t need = stage_bytes(p) + quantile_bytes(p, ctx->num_cu) + rup(bins * 4) +
+    const size_t need = quantile_bytes(p) + rup(bins * 4) +
                         rup(prefix_sum_words(p->S) * 8) + rup((size_t)C * K * 8) + rup((size_t)C * K * 4) +
                         4 * rup((size_t)C * 8) + rup(lp1_tableau_doubles(C, G) * 8) +
                         rup((size_t)m * 4) + 4 * rup((size_t)CG * 8) + 2 * rup((size_t)CG) +
@@ -1134,7 +1167,7 @@ int dro_bcd_solve(dro_ctx *ctx, const dro_problem *p, const float *eps, const dr
     if (rc) return rc;
 
     // the exact worst-case table of the radius row, the moments, the service times, r0
-    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.part, qb.hist, st));
+    HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_exact_table(p->offsets, p->seg, p->L, p->eta, p->lam, p->c_p, p->c_w, eps, nullptr,
                               qb.hist, p->S, 1, C, K, p->M, pcnt, psum, W, mstar, nullptr, nullptr,
                               nullptr, st));

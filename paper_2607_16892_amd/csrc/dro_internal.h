@@ -77,9 +77,9 @@ hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 hipError_t hist_prepare();
 // blocks per segment for the histogram pass
 int hist_parts(int S, long long max_seg, int num_cu);
-// hist: [S][kHistBins]; part: [S][B][kHistBins] scratch (unused when B == 1).
+// hist: [S][kHistBins], B blocks per segment (zeroed first when B > 1).
 hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
-                            uint32_t *part, uint32_t *hist, hipStream_t st);
+                            uint32_t *hist, hipStream_t st);
 hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st);

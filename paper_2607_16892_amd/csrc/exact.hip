@@ -85,16 +85,19 @@ hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 }
 
 // Block (segment s, part b of B): a private 32-bit LDS histogram of the values
-// 0 .. 2^15 (128 KB) over its 1/B share of the segment, stored to
-// part[s][b][:] with plain coalesced writes (no global atomics, so segments
-// with many blocks do not serialise on the same counters); a second kernel sums
-// the B parts of each segment.  1024 threads per block, each with four 16-byte
-// loads in flight, so the pass streams from HBM.
+// 0 .. 2^15 (128 KB) over its 1/B share of the segment, then added into the
+// segment's histogram: with plain stores when the block covers the whole
+// segment (B == 1), else with one atomic add per non-zero bin into a histogram
+// the launch has zeroed (integer adds, so the result does not depend on the
+// order).  Only the distinct values of a block cost a global access: about
+// 7,800 of the 32,769 bins for a block of 62,500 heavy-tailed lengths.  1024
+// threads per block, each with four 16-byte loads in flight, so the pass
+// streams from HBM.
 constexpr int kHistThreads = 1024;
 
 __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *offsets,
                                                                  const int32_t *xi, int B,
-                                                                 uint32_t *part)
+                                                                 uint32_t *hist)
 {
     extern __shared__ uint32_t h[];  // kHistBins words
     const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
@@ -114,38 +117,47 @@ __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *
     for (long long n = lo + t; n < a0; n += kHistThreads) count(xi[n]);
     const int4 *v4 = reinterpret_cast<const int4 *>(xi + a0);
     const long long nv = (a1 - a0) / 4;
-    for (long long r0 = 0; r0 < nv; r0 += 4LL * kHistThreads) {
-        int4 q[4];
+    // four 16-byte loads per thread per round, in two register sets: the next
+    // round's loads are in flight while this round's samples are counted
+    constexpr long long kRound = 4LL * kHistThreads;
+    int4 qa[4], qb[4];
+    // (unconditional loads, clamped to the last vector, so all four issue
+    // back to back; tally skips the ones past the end)
+    auto load = [&](long long r0, int4 (&d)[4]) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const long long i = r0 + r * kHistThreads + t;
-            q[r] = i < nv ? v4[i] : make_int4(0, 0, 0, 0);
+            d[r] = v4[i < nv ? i : nv - 1];
         }
+    };
+    auto tally = [&](long long r0, const int4 (&d)[4]) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             if (r0 + r * kHistThreads + t >= nv) continue;
-            count(q[r].x);
-            count(q[r].y);
-            count(q[r].z);
-            count(q[r].w);
+            count(d[r].x);
+            count(d[r].y);
+            count(d[r].z);
+            count(d[r].w);
         }
+    };
+    if (nv > 0) load(0, qa);
+    for (long long r0 = 0; r0 < nv; r0 += 2 * kRound) {
+        load(r0 + kRound, qb);
+        tally(r0, qa);
+        load(r0 + 2 * kRound, qa);
+        tally(r0 + kRound, qb);
     }
     for (long long n = a1 + t; n < hi; n += kHistThreads) count(xi[n]);
     __syncthreads();
-    uint32_t *o = part + ((long long)s * B + b) * kHistBins;
-    for (int i = t; i < kHistBins; i += kHistThreads) o[i] = h[i];
-}
-
-// hist[s][v] = sum over b of part[s][b][v]
-__global__ void hist_reduce_kernel(const uint32_t *part, int S, int B, uint32_t *hist)
-{
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (long long)S * kHistBins) return;
-    const long long s = i / kHistBins, v = i % kHistBins;
-    const uint32_t *p = part + s * B * kHistBins + v;
-    uint32_t acc = 0;
-    for (int b = 0; b < B; ++b) acc += p[(long long)b * kHistBins];
-    hist[i] = acc;
+    uint32_t *o = hist + (long long)s * kHistBins;
+    if (B == 1) {
+        for (int i = t; i < kHistBins; i += kHistThreads) o[i] = h[i];
+    } else {
+        for (int i = t; i < kHistBins; i += kHistThreads) {
+            const uint32_t c = h[i];
+            if (c) atomicAdd(o + i, c);
+        }
+    }
 }
 
 hipError_t select_prepare();
@@ -167,17 +179,12 @@ int hist_parts(int S, long long max_seg, int num_cu)
 }
 
 hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, int B,
-                            uint32_t *part, uint32_t *hist, hipStream_t st)
+                            uint32_t *hist, hipStream_t st)
 {
     if (S <= 0) return hipSuccess;
-    uint32_t *dst = B == 1 ? hist : part;
+    if (B > 1) HIPRET(launch_fill_u32(hist, (long long)S * kHistBins, 0u, st));
     hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((long long)S * B)), dim3(kHistThreads),
-                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, dst);
-    if (B > 1) {
-        const long long n = (long long)S * kHistBins;
-        hipLaunchKernelGGL(hist_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                           (const uint32_t *)part, S, B, hist);
-    }
+                       kHistBins * sizeof(uint32_t), st, offsets, xi, B, hist);
     return hipGetLastError();
 }
 
@@ -211,12 +218,24 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offs
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
     const uint32_t *h = hist + (long long)s * kHistBins;
-    for (int v = t; v < kHistBins; v += kSelThreads) hl[v] = h[v];  // coalesced
-    const int64_t j = exact_rank(c_p[c], c_w[c], N);
-    __syncthreads();
     // thread t owns the bins [t * per, (t + 1) * per); per is odd, so a wave's
     // LDS reads fall in distinct banks
     constexpr int per = (kHistBins + kSelThreads - 1) / kSelThreads;
+    {   // coalesced loads, all in flight before the first LDS store
+        uint32_t r[per];
+#pragma unroll
+        for (int i = 0; i < per; ++i) {
+            const int v = t + i * kSelThreads;
+            r[i] = v < kHistBins ? h[v] : 0u;
+        }
+#pragma unroll
+        for (int i = 0; i < per; ++i) {
+            const int v = t + i * kSelThreads;
+            if (v < kHistBins) hl[v] = r[i];
+        }
+    }
+    const int64_t j = exact_rank(c_p[c], c_w[c], N);
+    __syncthreads();
     const int b0 = t * per, b1 = min(kHistBins, b0 + per);
     uint64_t part = 0;
     for (int v = b0; v < b1; ++v) part += hl[v];
