@@ -54,11 +54,11 @@ PAPER_FLOPS_PER_EVAL = 7                 # 2 multiply-adds (4), a 3-way max (2),
 # stripped, identified by the hash prefix) and are reported as null for any
 # other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "83599eb12e88a3ba",
+    "dense_code_sha256_16": "097e05173d34a212",
     "workload": "mixture-16x1M",
-    "valu_instr_per_eval": 0.50659,    # SQ_INSTS_VALU x 64 / evaluations
-    "clock_ghz": 2.378,                # GRBM_GUI_ACTIVE / 8 XCDs / duration
-    "hbm_bytes_per_launch": 1406438647,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
+    "valu_instr_per_eval": 0.50464,    # SQ_INSTS_VALU x 64 / evaluations
+    "clock_ghz": 2.381,                # GRBM_GUI_ACTIVE / 8 XCDs / duration
+    "hbm_bytes_per_launch": 1406452004,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
     "source": "profiles/dense_kernel_mixture-16x1M_counters.md",
 }
 

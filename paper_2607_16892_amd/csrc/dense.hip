@@ -29,7 +29,7 @@
 // threshold t + 1 in both halves of b, it evaluates two terms of one
 // (k, m) pair in one single-rate VALU instruction.  Samples are staged in LDS
 // as 16-bit x + 1 (x <= 2^15, t clamped to [-1, L] or [0, L + 1], so both
-// fit), read back as wave-wide broadcasts of eight samples, and every lane
+// fit), read back as wave-wide broadcasts of sixteen samples, and every lane
 // keeps kTM thresholds and 32-bit sums of one grid point.  A 32-bit sum takes
 // at most kMaxSadSteps instructions before it is added to the 64-bit table.
 //
@@ -141,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
     }
 
     const bool row_ok = k < a.K;
-    // Sample codes 0 pad the last tile to whole groups of eight; each adds
+    // Sample codes 0 pad the last tile to whole groups of sixteen; each adds
     // t + 1 to a sum, which the flush takes off again.
     int pads = 0, steps = 0;
     auto flush = [&]() {
@@ -167,20 +167,19 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
     const uint4 *x4 = reinterpret_cast<const uint4 *>(xs);
     for (long long base = lo; base < hi; base += kTileN) {
         const int len = (int)min((long long)kTileN, hi - base);
-        const int len8 = (len + 7) & ~7;
-        if (steps + len8 / 2 > kMaxSadSteps) flush();
+        const int len16 = (len + 15) & ~15;
+        if (steps + len16 / 2 > kMaxSadSteps) flush();
         __syncthreads();
-        for (int i = t; i < len8; i += kThreads)
+        for (int i = t; i < len16; i += kThreads)
             xs[i] = i < len ? (uint16_t)(a.xi[base + i] + 1) : (uint16_t)0;
         __syncthreads();
-        pads += len8 - len;
-        steps += len8 / 2;
+        pads += len16 - len;
+        steps += len16 / 2;
 
-        // eight samples per step; the next eight are read while these are summed
-        const int n4 = len8 / 8;
-        uint4 v = x4[0];
-        for (int w = 0; w < n4; ++w) {
-            const uint4 nv = x4[min(w + 1, kTileN / 8 - 1)];
+        // sixteen samples (two broadcast LDS reads) per step
+        const int n8 = len16 / 16;
+        for (int w = 0; w < n8; ++w) {
+            const uint4 v = x4[2 * w], u = x4[2 * w + 1];
 #pragma unroll
             for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.x, thr[j], acc[j]);
 #pragma unroll
@@ -189,7 +188,14 @@ __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
             for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.z, thr[j], acc[j]);
 #pragma unroll
             for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.w, thr[j], acc[j]);
-            v = nv;
+#pragma unroll
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.x, thr[j], acc[j]);
+#pragma unroll
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.y, thr[j], acc[j]);
+#pragma unroll
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.z, thr[j], acc[j]);
+#pragma unroll
+            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.w, thr[j], acc[j]);
         }
     }
     if (steps > 0) flush();

@@ -15,7 +15,7 @@ namespace dro {
 // samples, staged through LDS as 16-bit codes x + 1.
 constexpr int kThreads = 256;
 constexpr int kTM = 32;
-constexpr int kTileN = 8192;          // samples staged per LDS tile (a multiple of 8)
+constexpr int kTileN = 8192;          // samples staged per LDS tile (a multiple of 16)
 constexpr int kMaxSadSteps = 65532;   // v_sad_u16 steps per 32-bit sum: each adds at most
                                       // 2 * 32770, and 65532 * 65540 < 2^32
 constexpr int kXcds = 8;              // accelerator complex dies of one MI355X (one L2 each)
