@@ -24,7 +24,7 @@ achieved rate over that ceiling.  The paper's three-candidate form would take
 separately, labelled as such, and is not executed work.
 
 `cpu_baseline` times the CPU oracle's dense fp64 evaluation on a bounded
-sample of the same workload (about 30 s), and the exact value-grouped oracle
+sample of the same workload (a quarter of one class, about 40 s), and the exact value-grouped oracle
 that validates parity on the whole workload.
 """
 from __future__ import annotations
@@ -330,8 +330,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mixture-16x1M")
-    ap.add_argument("--cpu-samples", type=int, default=200_000,
-                    help="samples of class 0 in the oracle's timed dense sample (about 30 s)")
+    ap.add_argument("--cpu-samples", type=int, default=250_000,
+                    help="samples of class 0 in the oracle's timed dense sample (a quarter of a "
+                         "class of the default workload, about 40 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-grouped-oracle", action="store_true",
                     help="skip timing the exact value-grouped oracle on the whole workload")
