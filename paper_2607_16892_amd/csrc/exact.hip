@@ -26,25 +26,6 @@ __device__ __forceinline__ int seg_of_x(const int32_t *seg, int c) { return seg 
         if (e_ != hipSuccess) return e_;             \
     } while (0)
 
-// phi in units of 2^-33: the three candidate points 0, x and L of Step 4.
-__device__ __forceinline__ int64_t phi_fix(int64_t eta, int64_t x, int64_t L, int64_t CP,
-                                           int64_t CW, int64_t G)
-{
-    const int64_t d = x - eta;
-    const int64_t q_x = d > 0 ? CP * d : CW * (-d);  // c_p (x-eta)^+ + c_w (eta-x)^+
-    const int64_t q_0 = CW * eta - G * x;            // Q(eta, 0) - g x
-    const int64_t q_L = CP * (L - eta) - G * (L - x);// Q(eta, L) - g (L - x)
-    const int64_t m = q_0 > q_L ? q_0 : q_L;
-    return q_x > m ? q_x : m;
-}
-
-__device__ __forceinline__ void add128(uint64_t &lo, uint64_t &hi, uint64_t blo, uint64_t bhi)
-{
-    const uint64_t r = lo + blo;
-    hi += bhi + (r < lo ? 1u : 0u);
-    lo = r;
-}
-
 // Exact S of one (class, grid point, multiplier), in units of 2^-33, from the
 // prefix counts cn[v] = #{x <= v} and sums sm[v] = sum{x : x <= v} of the
 // class's segment (N samples).  For 0 <= x, eta <= L the three candidates of

@@ -134,9 +134,9 @@ def _kink_workload():
     """Every sample sits just above the crossing point x0 of the two lines of phi.
 
     With c_w = c_p = 1.00055 lam_37 and eta = 30000 the crossing point is
-    x0 = 30007.49 while phi there is only about 6.5.  A kink rounded to fp32 in
-    absolute terms (error up to 2^-10 tokens at this size) would move S by
-    about 2e-4 relative; measured from eta it is exact to ~1e-7.
+    x0 = 30007.49 while phi there is only about 6.5: the sum rests on the
+    fractional part of x0 (the remainder r of the integer split), which an
+    approximate kink would get wrong by about 2e-4 relative.
     """
     from workloads import eta_grid, lam_grid
     from workloads.configs import Workload
