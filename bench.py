@@ -371,13 +371,15 @@ def main():
     S = torch.empty((w.C, w.K, w.M), dtype=torch.float64, device=dev)
     W = torch.empty((E, w.C, w.K), dtype=torch.float64, device=dev)
     m_star = torch.empty((E, w.C, w.K), dtype=torch.int32, device=dev)
+    q_value = torch.empty(w.C, dtype=torch.int32, device=dev)
+    q_rank = torch.empty(w.C, dtype=torch.int64, device=dev)
     outs = {}
 
     # every call goes to torch's current stream, where the events are recorded
     def step(ev=None):
         if ev:
             ev[0].record()
-        dro.class_quantile(ctx, prob)
+        dro.class_quantile(ctx, prob, q_value=q_value, q_rank=q_rank)
         if ev:
             ev[1].record()
         dro.dro_cost_eval(ctx, prob, eps, W=W, m_star=m_star, S=S)

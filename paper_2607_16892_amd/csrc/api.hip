@@ -629,15 +629,22 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     if (!q_value || !q_rank) return fail(ctx, DRO_EINVAL, "q_value and q_rank must be non-NULL");
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    rc = ensure_ws(ctx, quantile_bytes(p), st);
+    const int B = qhist_parts(p->S, sh.max_n, ctx->num_cu);
+    if ((long long)p->S * B > 0x7fffffffLL || (long long)p->C > 0x7fffffffLL)
+        return fail(ctx, DRO_ELIMIT, "S*B = %lld quantile blocks exceed 2^31 - 1", (long long)p->S * B);
+    const size_t rows = (size_t)p->S * B;
+    rc = ensure_ws(ctx, rup(rows * kQWords * 4) + rup(rows * kQBuckets * 4), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
-    return run_quantile(ctx, p, qb, q_value, q_rank, st);
+    uint32_t *fine = ar.take<uint32_t>(rows * kQWords);
+    uint32_t *coarse = ar.take<uint32_t>(rows * kQBuckets);
+    HIPCHK(launch_class_quantile(p->offsets, p->seg, p->xi, p->c_p, p->c_w, p->S, p->C, B, fine,
+                                 coarse, q_value, q_rank, st));
+    return DRO_OK;
 }
 
 int dro_exact_table(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *eps,

@@ -73,7 +73,7 @@ hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const
 // ---- quantile ----------------------------------------------------------------
 constexpr int kHistBins = 32769;   // values 0 .. 2^15
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st);
-// allows the histogram and quantile-select kernels their 128 KB of dynamic LDS (once per device)
+// allows the histogram and quantile kernels their 128 KB of dynamic LDS (once per device)
 hipError_t hist_prepare();
 // blocks per segment for the histogram pass
 int hist_parts(int S, long long max_seg, int num_cu);
@@ -83,6 +83,19 @@ hipError_t launch_histogram(const int64_t *offsets, const int32_t *xi, int S, in
 hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float *c_p,
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st);
+
+// ---- class_quantile (per-block packed histograms, then a select per class) ----
+constexpr int kQTop = 32768;              // largest sample value, 2^15
+constexpr int kQWords = kQTop / 2 + 1;    // packed 16-bit counts of the values 0 .. 2^15
+constexpr int kQBuckets = 256;            // coarse buckets of 128 values (the last also holds 2^15)
+constexpr long long kQMaxPart = 65535;    // samples per block, so every 16-bit count fits
+// blocks per segment: hist_parts, and enough that none holds more than kQMaxPart samples
+int qhist_parts(int S, long long max_seg, int num_cu);
+// fine: [S][B][kQWords] u32, coarse: [S][B][kQBuckets] u32 (scratch, fully written)
+hipError_t launch_class_quantile(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
+                                 const float *c_p, const float *c_w, int S, int C, int B,
+                                 uint32_t *fine, uint32_t *coarse, int32_t *q_value,
+                                 int64_t *q_rank, hipStream_t st);
 
 // ---- exact table (value counts and prefix sums) -------------------------------
 // The prefix pass works in chunks of 4096 bins.  A sum array holds the S x

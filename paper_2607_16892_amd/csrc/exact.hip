@@ -65,56 +65,38 @@ hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
     return hipGetLastError();
 }
 
-// Block (segment s, part b of B): a private 32-bit LDS histogram of the values
-// 0 .. 2^15 (128 KB) over its 1/B share of the segment, then added into the
-// segment's histogram: with plain stores when the block covers the whole
-// segment (B == 1), else with one atomic add per non-zero bin into a histogram
-// the launch has zeroed (integer adds, so the result does not depend on the
-// order).  Only the distinct values of a block cost a global access: about
-// 7,800 of the 32,769 bins for a block of 62,500 heavy-tailed lengths.  1024
-// threads per block, each with four 16-byte loads in flight, so the pass
-// streams from HBM.
-constexpr int kHistThreads = 1024;
-
-__global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *offsets,
-                                                                 const int32_t *xi, int B,
-                                                                 uint32_t *hist)
+// Calls count(x) for every sample of xi[lo, hi) handed to this thread of a
+// kThreadsT-thread block: an unaligned head (up to the first 16-byte aligned
+// address), a 16-byte body and a tail.  In the body every thread keeps eight
+// 16-byte loads in flight, in two register sets of four: the next round's
+// loads are issued before this round's samples are counted.  Body vector i
+// goes to thread i mod kThreadsT, so even and odd threads see alternate
+// vectors.
+template <int kThreadsT, class F>
+__device__ __forceinline__ void for_each_sample(const int32_t *xi, long long lo, long long hi, F &&count)
 {
-    extern __shared__ uint32_t h[];  // kHistBins words
-    const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
-    const long long n0 = offsets[s], N = offsets[s + 1] - n0;
-    const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
     const int t = threadIdx.x;
-    for (int i = t; i < kHistBins; i += kHistThreads) h[i] = 0;
-    __syncthreads();
-    auto count = [&](int v) {
-        v = v < 0 ? 0 : (v > kHistBins - 1 ? kHistBins - 1 : v);
-        atomicAdd(&h[v], 1u);
-    };
-    // unaligned head (up to the first 16-byte aligned address), 16-byte body, tail
     const long long mis = (long long)((reinterpret_cast<uintptr_t>(xi + lo) >> 2) & 3u);
     const long long a0 = min(hi, lo + ((4 - mis) & 3));
     const long long a1 = a0 + ((hi - a0) & ~3LL);
-    for (long long n = lo + t; n < a0; n += kHistThreads) count(xi[n]);
+    for (long long n = lo + t; n < a0; n += kThreadsT) count(xi[n]);
     const int4 *v4 = reinterpret_cast<const int4 *>(xi + a0);
     const long long nv = (a1 - a0) / 4;
-    // four 16-byte loads per thread per round, in two register sets: the next
-    // round's loads are in flight while this round's samples are counted
-    constexpr long long kRound = 4LL * kHistThreads;
+    constexpr long long kRound = 4LL * kThreadsT;
     int4 qa[4], qb[4];
     // (unconditional loads, clamped to the last vector, so all four issue
     // back to back; tally skips the ones past the end)
     auto load = [&](long long r0, int4 (&d)[4]) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const long long i = r0 + r * kHistThreads + t;
+            const long long i = r0 + r * kThreadsT + t;
             d[r] = v4[i < nv ? i : nv - 1];
         }
     };
     auto tally = [&](long long r0, const int4 (&d)[4]) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            if (r0 + r * kHistThreads + t >= nv) continue;
+            if (r0 + r * kThreadsT + t >= nv) continue;
             count(d[r].x);
             count(d[r].y);
             count(d[r].z);
@@ -128,7 +110,33 @@ __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *
         load(r0 + 2 * kRound, qa);
         tally(r0 + kRound, qb);
     }
-    for (long long n = a1 + t; n < hi; n += kHistThreads) count(xi[n]);
+    for (long long n = a1 + t; n < hi; n += kThreadsT) count(xi[n]);
+}
+
+// Block (segment s, part b of B): a private 32-bit LDS histogram of the values
+// 0 .. 2^15 (128 KB) over its 1/B share of the segment, then added into the
+// segment's histogram: with plain stores when the block covers the whole
+// segment (B == 1), else with one atomic add per non-zero bin into a histogram
+// the launch has zeroed (integer adds, so the result does not depend on the
+// order).  Only the distinct values of a block cost a global access: about
+// 7,800 of the 32,769 bins for a block of 62,500 heavy-tailed lengths.
+constexpr int kHistThreads = 1024;
+
+__global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *offsets,
+                                                                 const int32_t *xi, int B,
+                                                                 uint32_t *hist)
+{
+    extern __shared__ uint32_t h[];  // kHistBins words
+    const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
+    const long long n0 = offsets[s], N = offsets[s + 1] - n0;
+    const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
+    const int t = threadIdx.x;
+    for (int i = t; i < kHistBins; i += kHistThreads) h[i] = 0;
+    __syncthreads();
+    for_each_sample<kHistThreads>(xi, lo, hi, [&](int v) {
+        v = v < 0 ? 0 : (v > kHistBins - 1 ? kHistBins - 1 : v);
+        atomicAdd(&h[v], 1u);
+    });
     __syncthreads();
     uint32_t *o = hist + (long long)s * kHistBins;
     if (B == 1) {
@@ -141,14 +149,191 @@ __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *
     }
 }
 
+__device__ int64_t exact_rank(float cp, float cw, int64_t N);
+
+// ---- class_quantile: per-block histograms, then one select per class ----
+//
+// Block (segment s, part b of B, at most kQMaxPart samples) counts its share
+// in LDS with 16-bit counts packed two to a word (value v < 2^15 in word
+// v mod 2^14, low half for v < 2^14, high half above; 2^15 in the low half of
+// word 2^14), in two copies: even threads add into one, odd threads into the
+// other, which halves the lanes of one wave that meet on one LDS word when
+// short lengths repeat.  It then stores, with plain stores, the two copies'
+// sum (every count fits 16 bits, as the block holds at most 65,535 samples)
+// and its counts per coarse bucket of 128 values.  No global atomics: the
+// select reads the B rows of the bucket it needs.
+constexpr int kQThreads = 1024;
+
+__global__ __launch_bounds__(kQThreads) void qhist_kernel(const int64_t *offsets, const int32_t *xi,
+                                                          int B, uint32_t *fine, uint32_t *coarse)
+{
+    extern __shared__ uint32_t h[];  // 2 x kQWords words
+    const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
+    const long long n0 = offsets[s], N = offsets[s + 1] - n0;
+    const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
+    const int t = threadIdx.x;
+    for (int i = t; i < 2 * kQWords; i += kQThreads) h[i] = 0;
+    __syncthreads();
+    uint32_t *hc = h + (t & 1) * kQWords;
+    for_each_sample<kQThreads>(xi, lo, hi, [&](int v) {
+        v = v < 0 ? 0 : (v > kQTop ? kQTop : v);
+        // bit 14 of v selects the half (v = 2^15 has it clear)
+        atomicAdd(&hc[v < kQTop ? (v & (kQTop / 2 - 1)) : kQTop / 2], 1u << ((v >> 10) & 16));
+    });
+    __syncthreads();
+    uint32_t *out = fine + (long long)blockIdx.x * kQWords;
+    for (int w = t; w < kQWords; w += kQThreads) {
+        const uint32_t c = h[w] + h[kQWords + w];
+        h[w] = c;
+        out[w] = c;
+    }
+    __syncthreads();
+    // thread t: words [16 t, 16 t + 16), i.e. the values 16 t .. 16 t + 15
+    // (low halves, bucket t / 8) and 2^14 + 16 t .. (high halves, bucket
+    // 128 + t / 8); the reads start at a thread-dependent word to spread banks
+    static_assert(kQThreads * 16 == kQTop / 2, "one thread per 16 words");
+    uint32_t slo = 0, shi = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const uint32_t c = h[16 * t + ((i + t) & 15)];
+        slo += c & 0xffffu;
+        shi += c >> 16;
+    }
+    for (int d = 1; d < 8; d <<= 1) {
+        slo += __shfl_xor(slo, d, 64);
+        shi += __shfl_xor(shi, d, 64);
+    }
+    uint32_t *co = coarse + (long long)blockIdx.x * kQBuckets;
+    if ((t & 7) == 0) {
+        co[t >> 3] = slo;
+        // the last bucket also holds the value 2^15
+        co[128 + (t >> 3)] = shi + (t == kQThreads - 8 ? (h[kQTop / 2] & 0xffffu) : 0u);
+    }
+}
+
+// Block per class c (segment s): the coarse counts of the B parts summed per
+// bucket, the bucket holding the exact rank j, then the counts of its values
+// summed over the parts, and the value where the cumulative count reaches j.
+// Every thread issues its share of the B rows' loads together.
+__global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offsets,
+                                                            const int32_t *seg, const float *c_p,
+                                                            const float *c_w, const uint32_t *fine,
+                                                            const uint32_t *coarse, int B,
+                                                            int32_t *q_value, int64_t *q_rank)
+{
+    constexpr int kG = kQThreads / kQBuckets;  // row groups of the coarse sum
+    constexpr int kF = 129;                    // values of a bucket (the last adds 2^15)
+    constexpr int kFG = kQThreads / 128;       // row groups of the fine sum
+    __shared__ uint32_t part[kG][kQBuckets];
+    __shared__ uint32_t fpart[kFG][kF];
+    __shared__ uint32_t wsum[kQBuckets / 64];
+    __shared__ int sel;
+    __shared__ long long sel_below;
+    const int c = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int s = seg_of_x(seg, c);
+    const int64_t N = offsets[s + 1] - offsets[s];
+    const int64_t j = exact_rank(c_p[c], c_w[c], N);
+    const uint32_t *cs = coarse + (long long)s * B * kQBuckets;
+    const uint32_t *fs = fine + (long long)s * B * kQWords;
+    {
+        const int q = t % kQBuckets, g = t / kQBuckets;
+        uint32_t a = 0;
+        int bb = g;
+        for (; bb + 3 * kG < B; bb += 4 * kG) {
+            const uint32_t x0 = cs[(long long)bb * kQBuckets + q];
+            const uint32_t x1 = cs[(long long)(bb + kG) * kQBuckets + q];
+            const uint32_t x2 = cs[(long long)(bb + 2 * kG) * kQBuckets + q];
+            const uint32_t x3 = cs[(long long)(bb + 3 * kG) * kQBuckets + q];
+            a += (x0 + x1) + (x2 + x3);
+        }
+        for (; bb < B; bb += kG) a += cs[(long long)bb * kQBuckets + q];
+        part[g][q] = a;
+    }
+    if (t == 0) sel = -1;
+    __syncthreads();
+    // inclusive scan of the bucket totals (threads 0 .. 255), then the bucket
+    // whose range of ranks holds j
+    uint32_t tot = 0, incl = 0;
+    if (t < kQBuckets) {
+#pragma unroll
+        for (int g = 0; g < kG; ++g) tot += part[g][t];
+        incl = tot;
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t o = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += o;
+        }
+        if (lane == 63) wsum[wave] = incl;
+    }
+    __syncthreads();
+    if (t < kQBuckets) {
+        for (int w = 0; w < wave; ++w) incl += wsum[w];
+        const int64_t before = (int64_t)(incl - tot);
+        if (before < j && j <= (int64_t)incl) {
+            sel = t;
+            sel_below = before;
+        }
+    }
+    __syncthreads();
+    const int bk = sel;  // j is in [1, N] and the totals sum to N, so one bucket holds it
+    if (bk < 0) return;
+    const int v0 = bk < 128 ? 128 * bk : kQTop / 2 + 128 * (bk - 128);
+    {
+        // thread t: value v0 + t mod 128 over the rows t / 128, t / 128 + kFG, ...;
+        // threads of the first group also count 2^15 in the last bucket
+        const int o = t % 128, g = t / 128;
+        const int v = v0 + o;
+        const int w = v & (kQTop / 2 - 1), sh = (v >> 10) & 16;
+        const bool top = bk == kQBuckets - 1 && o == 0;
+        uint32_t a = 0, a_top = 0;
+        int bb = g;
+        for (; bb + 3 * kFG < B; bb += 4 * kFG) {
+            const uint32_t x0 = fs[(long long)bb * kQWords + w];
+            const uint32_t x1 = fs[(long long)(bb + kFG) * kQWords + w];
+            const uint32_t x2 = fs[(long long)(bb + 2 * kFG) * kQWords + w];
+            const uint32_t x3 = fs[(long long)(bb + 3 * kFG) * kQWords + w];
+            a += ((x0 >> sh) & 0xffffu) + ((x1 >> sh) & 0xffffu) + ((x2 >> sh) & 0xffffu) +
+                 ((x3 >> sh) & 0xffffu);
+        }
+        for (; bb < B; bb += kFG) a += (fs[(long long)bb * kQWords + w] >> sh) & 0xffffu;
+        if (top)
+            for (int r = g; r < B; r += kFG) a_top += fs[(long long)r * kQWords + kQTop / 2] & 0xffffu;
+        fpart[g][o] = a;
+        if (o == 0) fpart[g][128] = a_top;
+    }
+    __syncthreads();
+    // scan over the bucket's 129 value slots (threads 0 .. 255; slot 128 is 2^15)
+    uint32_t f = 0, fin = 0;
+    if (t < kQBuckets) {
+        if (t < kF)
+#pragma unroll
+            for (int g = 0; g < kFG; ++g) f += fpart[g][t];
+        fin = f;
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t o = __shfl_up(fin, d, 64);
+            if (lane >= d) fin += o;
+        }
+        if (lane == 63) wsum[wave] = fin;
+    }
+    __syncthreads();
+    if (t < kF) {
+        for (int w = 0; w < wave; ++w) fin += wsum[w];
+        const int64_t before = sel_below + (int64_t)(fin - f);
+        if (before < j && j <= before + (int64_t)f) q_value[c] = t < 128 ? v0 + t : kQTop;
+    }
+    if (t == 0) q_rank[c] = j;
+}
+
 hipError_t select_prepare();
+hipError_t qhist_prepare();
 
 hipError_t hist_prepare()
 {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(histogram_kernel),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)(kHistBins * sizeof(uint32_t)));
-    return e != hipSuccess ? e : select_prepare();
+    if (e != hipSuccess) return e;
+    const hipError_t e2 = select_prepare();
+    return e2 != hipSuccess ? e2 : qhist_prepare();
 }
 
 int hist_parts(int S, long long max_seg, int num_cu)
@@ -261,6 +446,32 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
 {
     hipLaunchKernelGGL(select_kernel, dim3(C), dim3(kSelThreads), kHistBins * sizeof(uint32_t), st,
                        offsets, seg, c_p, c_w, hist, q_value, q_rank);
+    return hipGetLastError();
+}
+
+hipError_t qhist_prepare()
+{
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(qhist_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)(2 * kQWords * sizeof(uint32_t)));
+}
+
+int qhist_parts(int S, long long max_seg, int num_cu)
+{
+    const long long need = (max_seg + kQMaxPart - 1) / kQMaxPart;
+    return (int)std::max((long long)hist_parts(S, max_seg, num_cu), std::max(1LL, need));
+}
+
+hipError_t launch_class_quantile(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
+                                 const float *c_p, const float *c_w, int S, int C, int B,
+                                 uint32_t *fine, uint32_t *coarse, int32_t *q_value,
+                                 int64_t *q_rank, hipStream_t st)
+{
+    hipLaunchKernelGGL(qhist_kernel, dim3((unsigned)((long long)S * B)), dim3(kQThreads),
+                       2 * kQWords * sizeof(uint32_t), st, offsets, xi, B, fine, coarse);
+    HIPRET(hipGetLastError());
+    hipLaunchKernelGGL(qselect_kernel, dim3((unsigned)C), dim3(kQThreads), 0, st, offsets, seg, c_p,
+                       c_w, fine, coarse, B, q_value, q_rank);
     return hipGetLastError();
 }
 
