@@ -54,11 +54,11 @@ PAPER_FLOPS_PER_EVAL = 7                 # 2 multiply-adds (4), a 3-way max (2),
 # stripped, identified by the hash prefix) and are reported as null for any
 # other code or workload.
 DENSE_COUNTERS = {
-    "dense_code_sha256_16": "097e05173d34a212",
+    "dense_code_sha256_16": "6553b8bf47eb1db9",
     "workload": "mixture-16x1M",
-    "valu_instr_per_eval": 0.50464,    # SQ_INSTS_VALU x 64 / evaluations
-    "clock_ghz": 2.381,                # GRBM_GUI_ACTIVE / 8 XCDs / duration
-    "hbm_bytes_per_launch": 1406452004,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
+    "valu_instr_per_eval": 0.50312,    # SQ_INSTS_VALU x 64 / evaluations
+    "clock_ghz": 2.371,                # GRBM_GUI_ACTIVE / 8 XCDs / duration
+    "hbm_bytes_per_launch": 222985011,  # FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 (copy-calibrated)
     "source": "profiles/dense_kernel_mixture-16x1M_counters.md",
 }
 
@@ -66,8 +66,8 @@ DENSE_COUNTERS = {
 def dense_code_hash() -> str:
     """Hash of the dense kernel's code, of its constants (the dense section of
     csrc/dro_internal.h) and of its launch plan (the plan constants and the
-    plan_dense function of csrc/api.hip, which set the number of sample slices
-    and so the atomic flush traffic), comments and whitespace removed."""
+    plan_dense function of csrc/api.hip, which set the slices and the grid),
+    comments and whitespace removed."""
     import hashlib
     import re
 
@@ -81,8 +81,9 @@ def dense_code_hash() -> str:
     consts = [ln for ln in hdr[:i].splitlines() if "constexpr" in ln]
     api = code("api.hip")
     plan_consts = [ln for ln in api.splitlines()
-                   if any(f"constexpr long long {k} " in ln for k in ("kMinWaves", "kMinSlice",
-                                                                      "kMaxSlices"))]
+                   if any(f"constexpr long long {k} " in ln for k in ("kDirectSampleTiles", "kSlicesPerBlock",
+                                                                      "kMaxSliceN", "kBalanceSliceN",
+                                                                      "kMinSliceN", "kMaxDirectSlices"))]
     i = api.index("DensePlan plan_dense(")
     plan = api[i:api.index("return pl;", i)]
     text = code("dense.hip") + "\n" + "\n".join(consts + plan_consts) + "\n" + plan
@@ -508,9 +509,10 @@ def main():
                      "traffic_note": "algorithmic bytes = the int32 samples read once plus the "
                                      "fp64 S table written once; traffic = copy-calibrated "
                                      "FETCH_SIZE + WRITE_SIZE of the committed counter profile: "
-                                     "the samples are fetched about once, and each block adds its "
-                                     "exact sums to the table with one 64-bit atomic per pair, "
-                                     "about 8 bytes of write traffic each",
+                                     "the samples are fetched about once, and a block adds a "
+                                     "tile's exact sums to the table with one 64-bit atomic per "
+                                     "pair each time it leaves that tile (about 2.3 times per "
+                                     "pair), about 8 bytes of write traffic each",
                      "launch_ms": dense_ms, "launch_ms_median": float(np.median(launch_times)),
                      "launch_ms_min": float(np.min(launch_times)), "evals_per_launch": evals,
                      "launch_note": "HIP events around dro_cost_eval on its stream: the dense "

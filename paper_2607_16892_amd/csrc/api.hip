@@ -181,25 +181,34 @@ int check_problem(dro_ctx *ctx, const dro_problem *p, Shape *sh)
     return DRO_OK;
 }
 
-// Tiles of kTM pairs per lane; the samples of every class are split into the
-// same P slices (P <= 64, and the largest class's slices hold at least
-// kMinSlice samples; a smaller class's may be short or empty, which adds
-// zero), each handled by its own blocks, which add their exact integer sums
-// into one table.  P is the smallest whose grid fills its last wave of
-// resident blocks (CUs x blocks per CU) to at least 97 % and runs at least
-// kMinWaves such waves; failing that, the well-filled P with the most waves,
-// else the best-filled P.  Each block adds its sums with one 64-bit atomic
-// per pair, so the flushes cost P x C x K x M atomics (8 bytes of memory
-// traffic each); short blocks keep the end of the launch from waiting on a
-// few long ones.  Measured on 16 x 1e6 samples (K = 2048, M = 256): 4 waves
-// of blocks ran 1.7 % slower than 16, and 16 to 48 waves ran within 0.5 % of
-// each other, so 16 halves the flushes of 32 at no cost.
+// Tiles of kTM pairs per lane; each tile's samples are split into P slices.
+// A problem with at least kDirectSampleTiles (tile, sample) terms per resident
+// block runs the persistent grid that claims slices (see dense.hip).  There P
+// is the largest of three needs: slices of at most kMaxSliceN samples, so that
+// the last ones are short; about kSlicesPerBlock slices per resident block, so
+// that the issue priorities keep the blocks of a compute unit in step and the
+// blocks still finding work near the end keep every unit full (slices down to
+// kBalanceSliceN samples); and one slice for every resident block (slices down
+// to kMinSliceN samples).  Measured on 16 x 1e6 samples (K = 2048, M = 256,
+// 1024 resident blocks): P = 16 (62,500-sample slices) ran 0.3 % faster than
+// the launch of 20,480 short blocks it replaced, P = 31 0.2 % slower and
+// P = 8 2.5 % slower.
+// A smaller problem (of at most 2^22 blocks) runs one block per slice instead
+// (direct mode): a run's set-up (its thresholds, claims, the search for work)
+// is then not small beside its work.  P is the smallest whose grid fills its
+// last wave of resident blocks to at least 97 %, else the best-filled P
+// (P <= 64, slices of at least kMinSliceN samples): on 4 x 1e5 samples
+// (K = 512, M = 128) one full wave of blocks (P = 32) ran 3 % faster than two
+// (P = 64) and 22 % faster than four.
 // The kernels index with the host-validated offsets and segment map: both are
 // copied into the workspace at the start of every call, so device data that
 // disagrees with the host copies can never steer a kernel outside xi.
-constexpr long long kMinWaves = 16;
-constexpr long long kMinSlice = 64;
-constexpr long long kMaxSlices = 64;
+constexpr long long kDirectSampleTiles = 65536;
+constexpr long long kSlicesPerBlock = 16;
+constexpr long long kMaxSliceN = 65536;
+constexpr long long kBalanceSliceN = 512;
+constexpr long long kMinSliceN = 64;
+constexpr long long kMaxDirectSlices = 64;
 
 size_t stage_bytes(const dro_problem *p)
 {
@@ -272,38 +281,65 @@ DensePlan plan_dense(int C, int K, int M, long long max_n, int num_cu, int bpc)
     pl.tiles_k = (K + pl.lanes_k - 1) / pl.lanes_k;
     pl.tiles_m = (M + kTM * pl.lanes_m - 1) / (kTM * pl.lanes_m);
     pl.tiles = pl.tiles_k * pl.tiles_m;
-    pl.group = std::min(pl.tiles, kTileGroup);
-    const long long base = (long long)C * pl.tiles;
-    const long long cap = (long long)num_cu * std::max(bpc, 1);
-    const long long maxP = std::max(1LL, std::min(kMaxSlices, max_n / kMinSlice));
-    long long fillP = 1, wellP = 0;
-    double best = -1.0;
-    for (long long P = 1; P <= maxP; ++P) {
-        const long long n = base * P;
-        const long long waves = (n + cap - 1) / cap;
-        const double fill = (double)n / (double)(waves * cap);
-        if (fill > best + 1e-9) {
-            best = fill;
-            fillP = P;
+    const long long T = (long long)C * pl.tiles;
+    const long long slots = (long long)num_cu * std::max(bpc, 1);
+    if (T * max_n < kDirectSampleTiles * slots && T * kMaxDirectSlices <= (1LL << 22)) {
+        const long long maxP = std::max(1LL, std::min(kMaxDirectSlices, max_n / kMinSliceN));
+        long long fillP = 1;
+        double best = -1.0;
+        for (long long P = 1; P <= maxP; ++P) {
+            const long long n = T * P;
+            const long long waves = (n + slots - 1) / slots;
+            const double fill = (double)n / (double)(waves * slots);
+            if (fill > best + 1e-9) {
+                best = fill;
+                fillP = P;
+            }
+            if (fill >= 0.97) break;
         }
-        if (fill >= 0.97) {
-            wellP = P;
-            if (waves >= kMinWaves) break;
-        }
+        pl.P = (int)fillP;
+        pl.direct = 1;
+        pl.blocks = T * pl.P;
+        return pl;
     }
-    pl.P = (int)(wellP > 0 ? wellP : fillP);
-    pl.blocks = base * pl.P;
+    const long long by_size = (max_n + kMaxSliceN - 1) / kMaxSliceN;
+    const long long by_balance = std::min((kSlicesPerBlock * slots + T - 1) / T, max_n / kBalanceSliceN);
+    const long long by_fill = std::min((slots + T - 1) / T, max_n / kMinSliceN);
+    long long P = std::max({1LL, by_size, by_balance, by_fill});
+    P = std::min(P, std::max(1LL, 0x7fffffffLL / T));  // T P claims fit the 32-bit counters
+    pl.P = (int)P;
+    pl.direct = 0;
+    pl.blocks = std::min(slots, T * P);
     return pl;
 }
 
+// Claim counters of a dense launch: one per tile and the total.
+size_t dense_claim_words(int C, int K, int M)
+{
+    const DensePlan pl = plan_dense(C, K, M, 1, 1, 1);
+    return (size_t)C * pl.tiles + 1;
+}
+
+// Host check of the dense entry points, before anything is enqueued: the
+// tiles and their claim counters are indexed in 32 bits.
+int check_dense(dro_ctx *ctx, const dro_problem *p)
+{
+    if ((long long)dense_claim_words(p->C, p->K, p->M) > 0x7fffffffLL)
+        return fail(ctx, DRO_ELIMIT, "C = %d classes of %zu dense tiles exceed 2^31 - 1 tiles", p->C,
+                    dense_claim_words(1, p->K, p->M) - 1);
+    return DRO_OK;
+}
+
 // Exact S into `S` ([C][K][M] doubles): the dense per-sample sums, then the
-// exact epilogue over the segments' prefix counts and sums (cnt, sum).
+// exact epilogue over the segments' prefix counts and sums (cnt, sum).  claim:
+// dense_claim_words scratch.
 int run_dense(dro_ctx *ctx, const dro_problem *p, double *S, const uint32_t *cnt,
-              const uint64_t *sum, const DensePlan &pl, hipStream_t st)
+              const uint64_t *sum, const DensePlan &pl, uint32_t *claim, hipStream_t st)
 {
     unsigned long long *R = reinterpret_cast<unsigned long long *>(S);
     const long long ckm = (long long)p->C * p->K * p->M;
-    HIPCHK(launch_zero_u64(R, ckm, st));
+    const long long T = (long long)p->C * pl.tiles;  // T P < 2^31: check_dense and plan_dense
+    HIPCHK(launch_zero_u64_u32(R, ckm, claim, T + 1, st));
     DenseArgs a{};
     a.offsets = p->offsets;
     a.seg = p->seg;
@@ -318,6 +354,7 @@ int run_dense(dro_ctx *ctx, const dro_problem *p, double *S, const uint32_t *cnt
     a.M = p->M;
     a.plan = pl;
     a.R = R;
+    a.claim = claim;
     HIPCHK(launch_dense(a, st));
     DenseFinishArgs f{};
     f.offsets = p->offsets;
@@ -380,13 +417,13 @@ bool finite_pos(float v) { return std::isfinite(v) && v > 0.0f; }
 bool in_limits(float v) { return v >= 0x1p-10f && v <= 0x1p7f; }
 
 // Scratch of one dense evaluation beyond S: the value histogram, the prefix
-// counts and sums (and, on the no-allocation path, the staged offsets and
-// segment map).
+// counts and sums, the slice claim counters (and, on the no-allocation path,
+// the staged offsets and segment map).
 size_t cost_eval_scratch_bytes(const dro_problem *p, bool with_stage)
 {
     const size_t bins = (size_t)p->S * kHistBins;
     return (with_stage ? stage_bytes(p) : 0) + quantile_bytes(p) + rup(bins * 4) +
-           rup(prefix_sum_words(p->S) * 8);
+           rup(prefix_sum_words(p->S) * 8) + rup(dense_claim_words(p->C, p->K, p->M) * 4);
 }
 
 // The dense evaluation over scratch taken from `ar` (the device must be
@@ -404,9 +441,10 @@ int run_cost_eval(dro_ctx *ctx, const dro_problem *p, const Shape &sh, int E, co
     const QuantBufs qb = take_quantile(ar, p, ctx->num_cu);
     uint32_t *cnt = ar.take<uint32_t>(bins);
     uint64_t *sum = ar.take<uint64_t>(prefix_sum_words(p->S));
+    uint32_t *claim = ar.take<uint32_t>(dense_claim_words(p->C, p->K, p->M));
     HIPCHK(launch_histogram(p->offsets, p->xi, p->S, qb.B, qb.hist, st));
     HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
-    rc = run_dense(ctx, p, Sbuf, cnt, sum, pl, st);
+    rc = run_dense(ctx, p, Sbuf, cnt, sum, pl, claim, st);
     if (rc) return rc;
     HIPCHK(launch_min_over_lambda(Sbuf, p->offsets, p->seg, p->lam, eps, E, p->C, p->K, p->M, W,
                                   m_star, st));
@@ -558,6 +596,7 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
     if (rc) return rc;
     if (E <= 0 || !eps || !W) return fail(ctx, DRO_EINVAL, "E must be > 0 and eps, W non-NULL");
     if ((rc = check_rows(ctx, E, p->C))) return rc;
+    if ((rc = check_dense(ctx, p))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const size_t ckm = (size_t)p->C * p->K * p->M;
@@ -585,6 +624,7 @@ int dro_cost_eval_noalloc(dro_ctx *ctx, const dro_problem *p, int32_t E, const f
         return fail(ctx, DRO_ELIMIT,
                     "the problem needs %zu bytes of scratch; the no-allocation array holds %zu",
                     need, (size_t)DRO_NOALLOC_SCRATCH_BYTES);
+    if ((rc = check_dense(ctx, p))) return rc;
     ENTER_DEVICE(ctx);
     Arena ar{(char *)ctx->scratch, 0};
     return run_cost_eval(ctx, p, sh, E, eps, W, m_star, S, ar, (hipStream_t)stream);
@@ -815,6 +855,7 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
         return fail(ctx, DRO_EINVAL, "a block-step argument or output is NULL");
     if (grp->G <= 0 || !grp->cap || !grp->conc || !std::isfinite(grp->kappa) || grp->kappa < 0.0f)
         return fail(ctx, DRO_EINVAL, "groups need G > 0, cap, conc and a finite kappa >= 0");
+    if ((rc = check_dense(ctx, p))) return rc;
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
     const int C = p->C;
@@ -823,7 +864,8 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     const size_t bins = (size_t)p->S * kHistBins;
     const size_t need = rup(ckm * 8) + quantile_bytes(p) + rup(bins * 4) +
                         rup(prefix_sum_words(p->S) * 8) + rup((size_t)C * p->K * 8) +
-                        rup((size_t)C * 8) + rup((size_t)C * 4);
+                        rup((size_t)C * 8) + rup((size_t)C * 4) +
+                        rup(dense_claim_words(C, p->K, p->M) * 4);
     rc = ensure_ws(ctx, need, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
@@ -838,13 +880,14 @@ int bcd_block_step(dro_ctx *ctx, const dro_problem *p, const float *eps, const d
     double *W = ar.take<double>((size_t)C * p->K);
     int64_t *q_rank = ar.take<int64_t>(C);
     int32_t *kcur = ar.take<int32_t>(C);
+    uint32_t *claim = ar.take<uint32_t>(dense_claim_words(C, p->K, p->M));
 
     rc = run_quantile(ctx, p, qb, out->q_value, q_rank, st);
     if (rc) return rc;
     // the quantile's value histogram also gives the prefix counts and sums of
     // the dense epilogue
     HIPCHK(launch_prefix(qb.hist, p->S, cnt, sum, st));
-    rc = run_dense(ctx, p, S, cnt, sum, pl, st);
+    rc = run_dense(ctx, p, S, cnt, sum, pl, claim, st);
     if (rc) return rc;
     HIPCHK(launch_min_over_lambda(S, p->offsets, p->seg, p->lam, eps, 1, C, p->K, p->M, W, nullptr,
                                   st));

@@ -30,13 +30,25 @@
 // (k, m) pair in one single-rate VALU instruction.  Samples are staged in LDS
 // as 16-bit x + 1 (x <= 2^15, t clamped to [-1, L] or [0, L + 1], so both
 // fit), read back as wave-wide broadcasts of sixteen samples, and every lane
-// keeps kTM thresholds and 32-bit sums of one grid point.  A 32-bit sum takes
-// at most kMaxSadSteps instructions before it is added to the 64-bit table.
+// keeps kTM thresholds and 32-bit sums of one grid point.  Every
+// kHalfSadSteps instructions the bit 2^31 of each sum moves into a 16-bit
+// carry in LDS, so a sum spans any number of samples without a flush.
 //
-// Reduction.  The samples of a class are split into P slices with their own
-// blocks; each block adds its exact integer sums to the [C][K][M] table with
-// 64-bit atomics.  Integer addition is associative, so the result does not
-// depend on the order the blocks finish in.
+// Reduction and schedule.  Each tile's samples are split into P slices, and
+// a persistent grid (every block resident) claims them with atomic counters:
+// a block first drains its own tiles, then the tiles of its XCD with the most
+// unclaimed slices, then any tile.  It keeps a tile's sums in registers over
+// all the consecutive slices it claims of that tile and adds them to the
+// [C][K][M] table with one 64-bit atomic per pair when it moves to another
+// tile (a run).  Integer addition is associative, so the table does not
+// depend on which block took which slice.  The wave arbiter of a compute unit
+// favours its oldest waves, which would let one of its blocks finish its tiles
+// far ahead of the others (and then take many short runs elsewhere); so at
+// every claim a block sets its waves' issue priority from its lead over the
+// average block, read from a counter of all claims.  Within a run, the claim
+// of the next slice is issued when a slice starts and read when it ends.
+#include <algorithm>
+
 #include "dro_internal.h"
 #include "fixed.h"
 
@@ -75,130 +87,291 @@ __device__ __forceinline__ long long slice_start(long long N, int p, int P)
 
 __global__ __launch_bounds__(kThreads) void dense_kernel(DenseArgs a)
 {
-    // The block's thresholds pass through LDS once (computed in a rolled loop),
-    // then the same memory holds the sample tiles.
+    // two staging buffers of kT samples (kT / kThreads prefetch registers per
+    // lane); at the start of a run the same memory passes the tile's
+    // thresholds from a rolled loop into registers
+    constexpr int kT = 4096;
     __shared__ __attribute__((aligned(16))) uint16_t xs[kTileN];
-    static_assert(kTileN >= kThreads * kTM, "the threshold table shares the sample tile");
+    __shared__ uint16_t carry[kTM * kThreads];
+    __shared__ int s_claim, s_prio;
+    __shared__ int s_best[kThreads / 64], s_left[kThreads / 64];
+    static_assert(kTileN >= kThreads * kTM, "the threshold table shares the sample buffers");
+    static_assert(kT % kThreads == 0 && kT % 16 == 0 && 2 * kT <= kTileN, "staging shape");
 
     const DensePlan pl = a.plan;
-    // Workgroups are dispatched to the XCDs in turn (block i to XCD i mod 8),
-    // so XCD x is given one contiguous run of logical blocks.  Logical blocks
-    // run through a class's tiles in groups of pl.group: all P slices of one
-    // group, then the next group.  The blocks resident on an XCD at one time
-    // then read a few sample slices and add into one group's part of the
-    // table, which both stay in that XCD's L2.
-    const long long nb = gridDim.x;
+    const int nb = (int)gridDim.x;
+    const int T = a.C * pl.tiles;  // tile tau: class tau / tiles, tile tau % tiles of it
+    // Workgroups are dispatched to the XCDs in turn (block i to XCD i mod 8), so
+    // XCD x is given one contiguous run of logical blocks, whose own tiles are
+    // one contiguous range [xt0, xt1): the blocks on an XCD read the samples of
+    // a few classes, which stay in its L2.
     const int xcd = (int)(blockIdx.x % kXcds);
-    const long long qx = nb / kXcds, rx = nb % kXcds;
-    long long b = xcd * qx + min((long long)xcd, rx) + blockIdx.x / kXcds;
-    const long long per_class = (long long)pl.tiles * pl.P;
-    const int c = (int)(b / per_class);
-    long long rem = b % per_class;
-    const int nfull = pl.tiles / pl.group;
-    int tile, p;
-    if (rem < (long long)nfull * pl.group * pl.P) {
-        const int g = (int)(rem / ((long long)pl.group * pl.P));
-        const int r2 = (int)(rem % ((long long)pl.group * pl.P));
-        p = r2 / pl.group;
-        tile = g * pl.group + r2 % pl.group;
-    } else {
-        const int r3 = (int)(rem - (long long)nfull * pl.group * pl.P);
-        const int gl = pl.tiles - nfull * pl.group;
-        p = r3 / gl;
-        tile = nfull * pl.group + r3 % gl;
-    }
-    const int tm = tile % pl.tiles_m, tk = tile / pl.tiles_m;
+    const int qx = nb / kXcds, rx = nb % kXcds;
+    const int xb0 = xcd * qx + min(xcd, rx);
+    const int xb1 = xb0 + qx + (xcd < rx ? 1 : 0);
+    const int b = xb0 + (int)(blockIdx.x / kXcds);
+    auto own = [&](int lb) { return (int)(((long long)lb * T) / nb); };
+    const int xt0 = own(xb0), xt1 = own(xb1);
+    int next_own = own(b);
+    const int own_end = own(b + 1);
 
     const int t = threadIdx.x;
     const int lm = t % pl.lanes_m, lk = t / pl.lanes_m;
     const int BM = kTM * pl.lanes_m;
-    const int k = tk * pl.lanes_k + lk;  // one grid point per lane
-    const int m0 = tm * BM + lm;         // multipliers m0 + j lanes_m
 
-    const int s = seg_of(a.seg, c);
-    const long long n_beg = a.offsets[s], N = a.offsets[s + 1] - n_beg;
-    const long long lo = n_beg + slice_start(N, p, pl.P);
-    const long long hi = n_beg + slice_start(N, p + 1, pl.P);
-
-    const float cpf = a.c_p[c], cwf = a.c_w[c];
-    const bool upper = cwf <= cpf;
-    const int64_t CP = fix33(cpf), CW = fix33(cwf);
-    const int L = a.L[c];
-    const int eta = a.eta[min(k, a.K - 1)];
-
-    for (int j = 0; j < kTM; ++j) {
-        const int m = min(m0 + j * pl.lanes_m, a.M - 1);
-        const PairLinesFix q = pair_lines_fix(CP, CW, fix33(a.lam[m]), eta, L);
-        xs[j * kThreads + t] = (uint16_t)(pair_kink(q, upper, L).tc + 1);
-    }
-    __syncthreads();
     uint32_t thr[kTM];  // (t + 1) in both 16-bit halves
     uint32_t acc[kTM];
 #pragma unroll
     for (int j = 0; j < kTM; ++j) {
-        thr[j] = (uint32_t)xs[j * kThreads + t] * 0x10001u;
         acc[j] = 0u;
+        carry[j * kThreads + t] = 0;
     }
-
-    const bool row_ok = k < a.K;
-    // Sample codes 0 pad the last tile to whole groups of sixteen; each adds
-    // t + 1 to a sum, which the flush takes off again.
+    int c = 0, k = 0, m0 = 0;
+    // Sample codes 0 pad the end of a slice to whole groups of sixteen; each
+    // adds t + 1 to a sum, which the flush takes off again.
     int pads = 0, steps = 0;
+
+    auto normalize = [&]() {
+        // (the address is hidden from the optimiser, which would otherwise keep
+        // the 32 carry addresses live across the sample loop)
+        int te = t;
+        asm volatile("" : "+v"(te));
+        uint16_t *cp = carry + te;
+#pragma unroll
+        for (int j = 0; j < kTM; ++j) {
+            cp[j * kThreads] += (uint16_t)(acc[j] >> 31);
+            acc[j] &= 0x7fffffffu;
+        }
+        steps = 0;
+    };
     auto flush = [&]() {
-        // Hiding the indices from the optimiser keeps it from holding the 32
-        // table addresses live across the sample loop.
-        int ke = k, me = m0;
-        asm volatile("" : "+v"(ke), "+v"(me));
-        unsigned long long *row = a.R + ((long long)c * a.K + ke) * a.M;
-        if (row_ok) {
+        int ke = k, me = m0, ce = c, te = t;
+        asm volatile("" : "+v"(ke), "+v"(me), "+v"(ce), "+v"(te));
+        unsigned long long *row = a.R + ((long long)ce * a.K + ke) * a.M;
+        uint16_t *cp = carry + te;
+        if (ke < a.K) {
 #pragma unroll
             for (int j = 0; j < kTM; ++j) {
                 const int m = me + j * pl.lanes_m;
-                if (m < a.M)
-                    atomicAdd(row + m, (unsigned long long)(acc[j] - (uint32_t)pads * (thr[j] & 0xffffu)));
+                uint32_t a32 = acc[j];
+                asm volatile("" : "+v"(a32));  // keeps the sums 32-bit through the sample loop
+                const unsigned long long tot = ((unsigned long long)cp[j * kThreads] << 31) + a32 -
+                                               (unsigned long long)pads * (thr[j] & 0xffffu);
+                if (m < a.M) atomicAdd(row + m, tot);
             }
         }
 #pragma unroll
-        for (int j = 0; j < kTM; ++j) acc[j] = 0u;
+        for (int j = 0; j < kTM; ++j) {
+            acc[j] = 0u;
+            cp[j * kThreads] = 0;
+        }
         pads = 0;
         steps = 0;
     };
-
-    const uint4 *x4 = reinterpret_cast<const uint4 *>(xs);
-    for (long long base = lo; base < hi; base += kTileN) {
-        const int len = (int)min((long long)kTileN, hi - base);
-        const int len16 = (len + 15) & ~15;
-        if (steps + len16 / 2 > kMaxSadSteps) flush();
-        __syncthreads();
-        for (int i = t; i < len16; i += kThreads)
-            xs[i] = i < len ? (uint16_t)(a.xi[base + i] + 1) : (uint16_t)0;
-        __syncthreads();
-        pads += len16 - len;
-        steps += len16 / 2;
-
-        // sixteen samples (two broadcast LDS reads) per step
-        const int n8 = len16 / 16;
-        for (int w = 0; w < n8; ++w) {
-            const uint4 v = x4[2 * w], u = x4[2 * w + 1];
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.x, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.y, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.z, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.w, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.x, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.y, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.z, thr[j], acc[j]);
-#pragma unroll
-            for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.w, thr[j], acc[j]);
+    // the thresholds of tile tau (lanes past K or M take the last valid pair;
+    // their sums are never stored)
+    auto start_run = [&](int tau) {
+        c = tau / pl.tiles;
+        const int tile = tau % pl.tiles;
+        const int tm = tile % pl.tiles_m, tk = tile / pl.tiles_m;
+        k = tk * pl.lanes_k + lk;
+        m0 = tm * BM + lm;
+        const float cpf = a.c_p[c], cwf = a.c_w[c];
+        const bool upper = cwf <= cpf;
+        const int64_t CP = fix33(cpf), CW = fix33(cwf);
+        const int L = a.L[c];
+        const int eta = a.eta[min(k, a.K - 1)];
+        // (four at a time: their multiplier loads overlap, and the 64-bit
+        // arithmetic of four pairs fits beside the live sums)
+#pragma unroll 4
+        for (int j = 0; j < kTM; ++j) {
+            const int m = min(m0 + j * pl.lanes_m, a.M - 1);
+            const PairLinesFix q = pair_lines_fix(CP, CW, fix33(a.lam[m]), eta, L);
+            xs[j * kThreads + t] = (uint16_t)(pair_kink(q, upper, L).tc + 1);
         }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kTM; ++j) thr[j] = (uint32_t)xs[j * kThreads + t] * 0x10001u;
+        __syncthreads();
+    };
+    // The samples xi[lo, hi) in buffers of kT: the next buffer's samples are
+    // loaded into registers while this one is evaluated, then stored; one
+    // barrier per buffer.
+    constexpr int kPer = kT / kThreads;
+    int32_t pf[kPer];
+    auto run_slice = [&](long long lo, long long hi) {
+        auto fetch = [&](long long base) {
+            // a block-uniform base and clamped 32-bit lane offsets: one
+            // address register per load and no branches
+            const int32_t *tp = a.xi + base;
+            const int len = (int)min((long long)kT, hi - base);
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) {
+                const int i = t + r * kThreads;
+                const int x = tp[min(i, len - 1)];
+                pf[r] = i < len ? x : -1;
+            }
+        };
+        auto put = [&](int buf) {
+            uint16_t *dst = xs + buf * kT;
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) dst[t + r * kThreads] = (uint16_t)(pf[r] + 1);
+        };
+        const int nbuf = (int)((hi - lo + kT - 1) / kT);
+        if (nbuf > 0) {
+            fetch(lo);
+            put(0);
+        }
+        __syncthreads();
+        for (int i = 0; i < nbuf; ++i) {
+            const long long base = lo + (long long)i * kT;
+            const int len = (int)min((long long)kT, hi - base);
+            const int len16 = (len + 15) & ~15;
+            if (steps + len16 / 2 > kHalfSadSteps) normalize();
+            if (i + 1 < nbuf) fetch(base + kT);
+            pads += len16 - len;
+            steps += len16 / 2;
+            // sixteen samples (two broadcast LDS reads) per step
+            const uint4 *x4 = reinterpret_cast<const uint4 *>(xs + (i & 1) * kT);
+            const int n8 = len16 / 16;
+            for (int w = 0; w < n8; ++w) {
+                const uint4 v = x4[2 * w], u = x4[2 * w + 1];
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.x, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.y, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.z, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(v.w, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.x, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.y, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.z, thr[j], acc[j]);
+#pragma unroll
+                for (int j = 0; j < kTM; ++j) acc[j] = __builtin_amdgcn_sad_u16(u.w, thr[j], acc[j]);
+            }
+            if (i + 1 < nbuf) put((i + 1) & 1);
+            __syncthreads();
+        }
+    };
+    // Issue priority from this block's lead over the average block: done is
+    // the number of slices it has claimed, g the number all blocks had claimed
+    // before its latest claim; 0 for a slice or more ahead, 3 for more than a
+    // slice behind.
+    int done = 0;
+    auto prio_of = [&](long long g) {
+        const long long lead = (long long)done * nb - g;  // in 1/nb slices
+        return lead >= nb ? 0 : (lead >= 0 ? 1 : (lead >= -nb ? 2 : 3));
+    };
+    auto set_prio = [&](int level) {
+        switch (level) {
+        case 0: __builtin_amdgcn_s_setprio(0); break;
+        case 1: __builtin_amdgcn_s_setprio(1); break;
+        case 2: __builtin_amdgcn_s_setprio(2); break;
+        default: __builtin_amdgcn_s_setprio(3); break;
+        }
+    };
+    // Claims the next slice of tile tau for the whole block and waits for it
+    // (block-uniform result: P or more means the tile is drained).
+    auto claim = [&](int tau) {
+        __syncthreads();
+        if (t == 0) {
+            s_claim = (int)atomicAdd(a.claim + tau, 1u);
+            s_prio = prio_of((long long)atomicAdd(a.claim + T, 1u));
+        }
+        __syncthreads();
+        return s_claim;
+    };
+    // The tile of [q0, q1) with the most unclaimed slices (-1 if none): every
+    // thread reads some counters, then a block-wide maximum (ties to the
+    // higher index).  Counters only grow, and the coherent reads see every
+    // completed claim, so a block that finds a tile drained never picks it
+    // again: the search ends.
+    auto most_left = [&](int q0, int q1) {
+        int best = -1, left = 0;
+        for (int q = q0 + t; q < q1; q += kThreads) {
+            const int r = pl.P - (int)__hip_atomic_load(a.claim + q, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+            if (r > left) {
+                left = r;
+                best = q;
+            }
+        }
+        for (int d = 32; d >= 1; d >>= 1) {
+            const int ob = __shfl_xor(best, d, 64), ol = __shfl_xor(left, d, 64);
+            if (ol > left || (ol == left && ob > best)) {
+                left = ol;
+                best = ob;
+            }
+        }
+        __syncthreads();
+        if ((t & 63) == 0) {
+            s_best[t >> 6] = best;
+            s_left[t >> 6] = left;
+        }
+        __syncthreads();
+        if (t == 0) {
+            int bb = s_best[0], bl = s_left[0];
+            for (int w = 1; w < kThreads / 64; ++w)
+                if (s_left[w] > bl || (s_left[w] == bl && s_best[w] > bb)) {
+                    bl = s_left[w];
+                    bb = s_best[w];
+                }
+            s_claim = bl > 0 ? bb : -1;
+        }
+        __syncthreads();
+        return s_claim;
+    };
+
+    if (pl.direct) {
+        // Small problems: the grid has a block per slice (slices of a tile on
+        // consecutive logical blocks) and the hardware hands blocks to compute
+        // units as they free up; no claims.
+        const int tau = b / pl.P, p = b % pl.P;
+        start_run(tau);
+        const int sg = seg_of(a.seg, c);
+        const long long n_beg = a.offsets[sg], N = a.offsets[sg + 1] - n_beg;
+        run_slice(n_beg + slice_start(N, p, pl.P), n_beg + slice_start(N, p + 1, pl.P));
+        flush();
+        return;
     }
-    if (steps > 0) flush();
+
+    // Runs: pick a tile and claim a slice of it; take its thresholds; evaluate
+    // its slices while claims on it succeed; add the sums to the table.
+    bool any_xcd = xt0 == 0 && xt1 == T;  // search every tile (this XCD's are drained)
+    for (;;) {
+        int tau = -1, p = pl.P;
+        while (p >= pl.P) {
+            if (next_own < own_end) {
+                tau = next_own++;
+            } else {
+                tau = any_xcd ? most_left(0, T) : most_left(xt0, xt1);
+                if (tau < 0) {
+                    if (any_xcd) break;
+                    any_xcd = true;
+                    continue;
+                }
+            }
+            p = claim(tau);
+        }
+        if (p >= pl.P) break;  // every slice has been claimed
+        ++done;
+        set_prio(s_prio);
+        start_run(tau);
+        const int sg = seg_of(a.seg, c);
+        const long long n_beg = a.offsets[sg], N = a.offsets[sg + 1] - n_beg;
+        for (;;) {
+            run_slice(n_beg + slice_start(N, p, pl.P), n_beg + slice_start(N, p + 1, pl.P));
+            p = claim(tau);
+            if (p >= pl.P) break;
+            ++done;
+            set_prio(s_prio);
+        }
+        flush();
+    }
 }
 
 int dense_blocks_per_cu()
@@ -215,16 +388,20 @@ hipError_t launch_dense(const DenseArgs &a, hipStream_t st)
     return hipGetLastError();
 }
 
-__global__ void fill_u64_kernel(unsigned long long *p, long long n)
+__global__ void zero_u64_u32_kernel(unsigned long long *p, long long n, uint32_t *q, long long nq)
 {
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = 0ull;
+    if (i < nq) q[i] = 0u;
 }
 
-hipError_t launch_zero_u64(unsigned long long *p, long long n, hipStream_t st)
+hipError_t launch_zero_u64_u32(unsigned long long *p, long long n, uint32_t *q, long long nq,
+                               hipStream_t st)
 {
-    if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(fill_u64_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n);
+    const long long m = std::max(n, nq);
+    if (m <= 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_u64_u32_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, st, p,
+                       n, q, nq);
     return hipGetLastError();
 }
 

@@ -10,24 +10,26 @@
 namespace dro {
 
 // ---- dense evaluation -------------------------------------------------------
-// Every lane owns one grid point and kTM multipliers; a 256-lane block covers
-// lanes_k x (kTM * lanes_m) pairs of one class and one slice of that class's
-// samples, staged through LDS as 16-bit codes x + 1.
+// Every lane owns one grid point and kTM multipliers; a 256-lane block covers a
+// tile of lanes_k x (kTM * lanes_m) pairs of one class.  The samples of each
+// tile are split into P slices.  A persistent grid of blocks claims slices
+// (its own tiles first, then other tiles' unclaimed slices) and keeps a
+// tile's sums in registers over consecutive slices of that tile.
 constexpr int kThreads = 256;
 constexpr int kTM = 32;
-constexpr int kTileN = 8192;          // samples staged per LDS tile (a multiple of 16)
-constexpr int kMaxSadSteps = 65532;   // v_sad_u16 steps per 32-bit sum: each adds at most
-                                      // 2 * 32770, and 65532 * 65540 < 2^32
+constexpr int kTileN = 8192;          // 16-bit LDS words of the staging buffers and the thresholds
+constexpr int kHalfSadSteps = 32766;  // v_sad_u16 steps between carries: a sum kept below 2^31
+                                      // takes 32766 more steps of at most 2 * 32770 below 2^32
 constexpr int kXcds = 8;              // accelerator complex dies of one MI355X (one L2 each)
-constexpr int kTileGroup = 64;        // tiles whose slices run together (block order)
 
 struct DensePlan {
     int lanes_m, lanes_k;  // lane grid inside a block
     int tiles_k, tiles_m;  // block tiles per class
     int tiles;             // tiles_k * tiles_m
-    int group;             // tiles per group of the block order, <= tiles
-    int P;                 // sample slices per class
-    long long blocks;      // C * tiles * P
+    int P;                 // sample slices per tile
+    int direct;            // 1: one block per slice, no claims (small problems)
+    long long blocks;      // direct: C * tiles * P; else the persistent grid,
+                           // min(resident blocks, C * tiles * P)
 };
 
 struct DenseArgs {
@@ -42,12 +44,15 @@ struct DenseArgs {
     int C, K, M;
     DensePlan plan;
     unsigned long long *R;  // [C][K][M] sums of |x - t| over the class's samples, zeroed first
+    uint32_t *claim;        // [C * tiles + 1] slice counters per tile, then the total; zeroed first
 };
 
 hipError_t launch_dense(const DenseArgs &a, hipStream_t st);
 // resident dense blocks per compute unit (occupancy of dense_kernel)
 int dense_blocks_per_cu();
-hipError_t launch_zero_u64(unsigned long long *p, long long n, hipStream_t st);
+// zeroes p[0, n) and q[0, nq)
+hipError_t launch_zero_u64_u32(unsigned long long *p, long long n, uint32_t *q, long long nq,
+                               hipStream_t st);
 
 // S from the dense kernel's sums and the segments' prefix counts and sums
 // (cnt, sum: [S][kHistBins], from launch_prefix), written over R as doubles.
