@@ -38,8 +38,9 @@
  *  - A ctx is not thread-safe: use one ctx per host thread / stream.
  *  - Exactness limits (DRO_ELIMIT when exceeded): 0 <= x, eta <= L <= 2^15,
  *    N_c <= 2^26 samples per class, every lam, c_p, c_w in [2^-10, 2^7];
- *    K <= 2^15 + 1 grid points, M <= 65536 multipliers, K * M < 2^31 pairs
- *    and E * C < 2^31 radius rows.
+ *    K <= 2^15 + 1 grid points, M <= 65536 multipliers, K * M < 2^31 pairs,
+ *    E * C < 2^31 radius rows, and (dense evaluation) fewer than 2^31 - 1
+ *    tiles of 8192 (k, m) pairs over all classes.
  *    Inside them every candidate of phi is a multiple of 2^-33 below 2^56, so
  *    the library evaluates every S exactly in 128-bit fixed point and rounds
  *    it to double once.
@@ -146,8 +147,8 @@ int dro_cost_eval(dro_ctx *ctx, const dro_problem *p, int32_t E, const float *ep
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, results and errors as dro_cost_eval, except that S is
  * required (the dense sums accumulate in it) and the scratch (the staged
- * offsets and segment map, the value histogram, the prefix counts and sums)
- * comes from a static device array of DRO_NOALLOC_SCRATCH_BYTES instead of
+ * offsets and segment map, the value histogram, the prefix counts and sums,
+ * the dense kernel's work counters, one per tile) comes from a static device array of DRO_NOALLOC_SCRATCH_BYTES instead of
  * the ctx workspace, so the call allocates nothing.  The scratch grows with
  * the number of sample segments, about 0.5 MB each: a problem that needs
  * more than the array (beyond about 60 segments) gets DRO_ELIMIT before any
