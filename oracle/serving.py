@@ -46,12 +46,15 @@ the paper leaves open marked "reading":
 Every double expression is written in a fixed order, one rounding per
 operation, as the library evaluates it.
 
-Pins: the P-K wait reduces to the M/M/1 wait, caching saves memory exactly
-when the concurrency exceeds the margin, the LP1 optimum (HiGHS) beats sampled
-feasible routings, the configuration scan equals brute force, and the LP2
-sweep equals the pinned block step (tests/test_oracle_pins.py, P20-P24).
-Beyond those, parity unpinned: the serving model follows readings of a model
-whose constants the paper does not print, in the same order as the library.
+Pins (tests/test_oracle_pins.py): the P-K wait reduces to the M/M/1 wait,
+caching saves memory exactly when the concurrency exceeds the margin, the LP1
+optimum (HiGHS) beats sampled feasible routings, the configuration scan equals
+brute force, and the LP2 sweep equals the pinned block step (P20-P24); the
+service-time moments, concurrencies, memory, waiting times and objective equal
+their formulas evaluated in exact rationals in another algebraic form (per
+sample value; E[S^2] / (2 E[S]) for the wait) (P25-P28).  What stays unpinned
+is the model itself: it follows readings of a model whose constants the paper
+does not print.
 """
 from __future__ import annotations
 

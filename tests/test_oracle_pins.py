@@ -783,3 +783,106 @@ def test_P18_mean_plus_spread_on_a_hand_worked_sample():
     row = dict(zip(policies.policy_names((0.0,)), eta[:, 0]))
     assert row["Mean"] == 4 and row["LP+1sigma"] == 8 and row["LP+2sigma"] == 12
     assert row["P90"] == 10 and row["Max"] == 20     # ceil(0.9 * 4) = 4th smallest
+
+
+# ---- P25-P28: the serving oracle's arithmetic against its formulas in exact
+# rationals, written in a different algebraic form (per sample value instead of
+# expanded moments, the textbook E[S^2] / (2 E[S]) form of the P-K wait), so a
+# dropped term, a wrong sign or divisor, or a swapped index fails whatever the
+# operation order of the fp64 code.
+
+def _q(v):
+    return F(float(v))
+
+
+def _close(a, b, rel):
+    a, b = F(float(a)), F(b)
+    return abs(a - b) <= F(rel) * max(abs(b), F(1, 10 ** 30))
+
+
+@pytest.mark.parametrize("seed", [31, 32])
+def test_P25_service_time_moments_in_rationals(seed):
+    # Sec. 3.1: on configuration g a request of class c with output length x
+    # takes A + B x, A = pp alpha Lin / Cc + NL tau t_ar, B = beta / Bc; T and ET2
+    # are its mean and second moment over the class's samples
+    from oracle import serving as osv
+    w, svc = _serving_tiny(seed)
+    T, ET2 = osv.service_times(svc, w)
+    for c in range(w.C):
+        vals, cnt = np.unique(w.samples_of(c), return_counts=True)
+        n = int(cnt.sum())
+        for g in range(svc.G):
+            A = (_q(svc.pp[g]) * _q(svc.alpha) * _q(svc.Lin[c]) / _q(svc.Cc[g])
+                 + _q(svc.NL) * _q(svc.tau[g]) * _q(svc.t_ar))
+            B = _q(svc.beta) / _q(svc.Bc[g])
+            t = sum(int(m) * (A + B * int(v)) for v, m in zip(vals, cnt)) / n
+            t2 = sum(int(m) * (A + B * int(v)) ** 2 for v, m in zip(vals, cnt)) / n
+            assert _close(T[c, g], t, 1e-14), (c, g)
+            assert _close(ET2[c, g], t2, 1e-14), (c, g)
+
+
+def test_P26_concurrency_and_memory_in_rationals():
+    # Little's law conc = lam T pi / z, and the KV tokens of Sec. 3.4:
+    # mem = (1 + kappa) sum_c conc_cg (Lin_c + eta_c - delta_cg Lpre_c) + sum_c delta_cg Lpre_c
+    from oracle import serving as osv
+    w, svc = _serving_tiny(33)
+    T, _ = osv.service_times(svc, w)
+    rng = np.random.default_rng(33)
+    pi = rng.uniform(0.0, 0.5, (w.C, svc.G))
+    z = np.array([1, 3, 2], np.int64)
+    eta_c = rng.integers(0, 600, w.C)
+    delta = (rng.random((w.C, svc.G)) < 0.5).astype(np.uint8)
+    conc = osv.concurrency(svc, T, pi, z)
+    mem = osv.memory(svc, T, pi, z, eta_c, delta)
+    for g in range(svc.G):
+        tot = F(0)
+        for c in range(w.C):
+            q = _q(svc.lam[c]) * _q(T[c, g]) * _q(pi[c, g]) / int(z[g])
+            assert _close(conc[c, g], q, 1e-15)
+            tot += (1 + _q(svc.kappa)) * q * (int(svc.Lin[c]) + int(eta_c[c])
+                                              - int(delta[c, g]) * int(svc.Lpre[c]))
+            tot += int(delta[c, g]) * int(svc.Lpre[c])
+        assert _close(mem[g], tot, 1e-13), g
+
+
+def test_P27_waiting_time_in_the_textbook_form():
+    # Pollaczek-Khinchin: Wq = u E[S^2] / (2 (1 - u) E[S]) with the service-time
+    # moments mixed by the routed arrival rates, u = mem / Mcap
+    from oracle import serving as osv
+    w, svc = _serving_tiny(34)
+    T, ET2 = osv.service_times(svc, w)
+    rng = np.random.default_rng(34)
+    pi = rng.uniform(0.05, 0.5, (w.C, svc.G))
+    z = np.array([2, 1, 1], np.int64)
+    mem = rng.uniform(0.1, 0.9, svc.G) * svc.Mcap.astype(np.float64)
+    Wq = osv.queue(svc, T, ET2, pi, z, mem)
+    for g in range(svc.G):
+        X = sum(_q(svc.lam[c]) * _q(pi[c, g]) for c in range(w.C))
+        es = sum(_q(svc.lam[c]) * _q(pi[c, g]) * _q(T[c, g]) for c in range(w.C)) / X
+        es2 = sum(_q(svc.lam[c]) * _q(pi[c, g]) * _q(ET2[c, g]) for c in range(w.C)) / X
+        u = _q(mem[g]) / _q(svc.Mcap[g])
+        assert _close(Wq[g], u * es2 / (2 * (1 - u) * es), 1e-12), g
+
+
+def test_P28_objective_in_rationals():
+    # the per-class cost of Sec. 3.3-3.4 summed with the arrival rates:
+    # lam (a W + sum_g pi c_gpu tau pp T + c_slo max(0, sum_g pi (Wq + T) - a D)
+    #      + (1 - a) c_rej), a = sum_g pi
+    from oracle import serving as osv
+    w, svc = _serving_tiny(35)
+    T, _ = osv.service_times(svc, w)
+    rng = np.random.default_rng(35)
+    Wc = rng.uniform(10.0, 3000.0, w.C)
+    for trial in range(4):
+        pi = rng.dirichlet(np.ones(svc.G + 1), w.C)[:, :svc.G]
+        Wq = rng.uniform(0.0, 30.0 if trial % 2 else 0.5, svc.G)
+        obj = osv.objective(svc, Wc, T, Wq, pi)
+        tot = F(0)
+        for c in range(w.C):
+            a = sum(_q(pi[c, g]) for g in range(svc.G))
+            gpu = sum(_q(pi[c, g]) * _q(svc.c_gpu) * int(svc.tau[g]) * int(svc.pp[g]) * _q(T[c, g])
+                      for g in range(svc.G))
+            slack = sum(_q(pi[c, g]) * (_q(Wq[g]) + _q(T[c, g])) for g in range(svc.G)) - a * _q(svc.D[c])
+            tot += _q(svc.lam[c]) * (a * _q(Wc[c]) + gpu + _q(svc.c_slo) * max(slack, F(0))
+                                     + (1 - a) * _q(svc.c_rej))
+        assert _close(obj, tot, 1e-12), trial
