@@ -460,45 +460,71 @@ hipError_t launch_dense_finish(const DenseFinishArgs &a, hipStream_t st)
     return hipGetLastError();
 }
 
-// One thread per (c, k); radii in groups of 8 so S[c,k,:] is read E/8 times.
-__global__ void min_over_lambda_kernel(const double *S, const int64_t *offsets, const int32_t *seg,
-                                       const float *lam, const float *eps, int E, int C, int K,
-                                       int M, double *W, int32_t *m_star)
+// One wave per (c, k) row.  The wave stages q_m = S[c,k,m] / N and lambda_m
+// for a chunk of multipliers in LDS (coalesced reads of the row, each quotient
+// computed once); then its 64 lanes split into g groups of 64/g, g the power of
+// two covering E (at most 64), group j taking radius e0 + j and its lanes the
+// multipliers m = part, part + 64/g, ... of the chunk.  Each lane keeps the
+// smallest J of its multipliers (the lowest m among equal values, as it visits
+// them in ascending order), then log2(64/g) shuffle steps take the smallest J
+// of the group, ties to the lowest m: the same J bits and the same lowest m as
+// a scan over m.
+constexpr int kMinWaves = 4;    // waves (rows) per block
+constexpr int kMinChunk = 256;  // multipliers staged per wave at a time
+
+__global__ __launch_bounds__(64 * kMinWaves) void min_over_lambda_kernel(
+    const double *S, const int64_t *offsets, const int32_t *seg, const float *lam, const float *eps,
+    int E, int C, int K, int M, double *W, int32_t *m_star)
 {
-    const long long ck = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (ck >= (long long)C * K) return;
+    __shared__ double2 st[kMinWaves][kMinChunk];  // (q_m, lambda_m)
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const long long ck = (long long)blockIdx.x * kMinWaves + w;
+    if (ck >= (long long)C * K) return;  // whole waves; no block barrier below
     const int c = (int)(ck / K), k = (int)(ck % K);
     const int s = seg_of(seg, c);
     const double N = (double)(offsets[s + 1] - offsets[s]);
     const double *row = S + ck * M;
-    for (int e0 = 0; e0 < E; e0 += 8) {
-        double best[8];
-        int bm[8];
-        double ev[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            best[q] = __builtin_inf();
-            bm[q] = 0;
-            ev[q] = (e0 + q < E) ? (double)eps[(long long)(e0 + q) * C + c] : 0.0;
-        }
-        for (int m = 0; m < M; ++m) {
-            const double lm = (double)lam[m];
-            const double q_ = __ddiv_rn(row[m], N);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const double J = __dadd_rn(__dmul_rn(lm, ev[q]), q_);
-                if (J < best[q]) {
-                    best[q] = J;
-                    bm[q] = m;
+    int lg = 0;  // log2 of the groups
+    while (lg < 6 && (1 << lg) < E) ++lg;
+    const int lp = 6 - lg;  // log2 of the lanes per group
+    const int part = lane & ((1 << lp) - 1), grp = lane >> lp;
+    double2 *q = st[w];
+    for (int e0 = 0; e0 < E; e0 += 1 << lg) {
+        const int e = e0 + grp;
+        const double ev = e < E ? (double)eps[(long long)e * C + c] : 0.0;
+        double best = __builtin_inf();
+        int bm = M;  // no multiplier yet: loses every comparison below
+        for (int m0 = 0; m0 < M; m0 += kMinChunk) {
+            const int mc = min(kMinChunk, M - m0);
+            if (e0 == 0 || M > kMinChunk) {  // else the one chunk is still staged
+                __builtin_amdgcn_wave_barrier();  // the last chunk's reads come first
+                for (int i = lane; i < mc; i += 64)
+                    q[i] = make_double2(__ddiv_rn(row[m0 + i], N), (double)lam[m0 + i]);
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            }
+            for (int i = part; i < mc; i += 1 << lp) {
+                const double2 v = q[i];
+                const double J = __dadd_rn(__dmul_rn(v.y, ev), v.x);
+                if (J < best) {
+                    best = J;
+                    bm = m0 + i;
                 }
             }
         }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            if (e0 + q >= E) break;
-            const long long o = ((long long)(e0 + q) * C + c) * K + k;
-            W[o] = best[q];
-            if (m_star) m_star[o] = bm[q];
+        for (int d = (1 << lp) >> 1; d >= 1; d >>= 1) {
+            const double ob = __shfl_xor(best, d, 64);
+            const int om = __shfl_xor(bm, d, 64);
+            if (ob < best || (ob == best && om < bm)) {
+                best = ob;
+                bm = om;
+            }
+        }
+        if (part == 0 && e < E) {
+            const long long o = ((long long)e * C + c) * K + k;
+            W[o] = best;
+            if (m_star) m_star[o] = bm;
         }
     }
 }
@@ -508,8 +534,8 @@ hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const
                                   double *W, int32_t *m_star, hipStream_t st)
 {
     const long long n = (long long)C * K;
-    hipLaunchKernelGGL(min_over_lambda_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                       S, offsets, seg, lam, eps, E, C, K, M, W, m_star);
+    hipLaunchKernelGGL(min_over_lambda_kernel, dim3((unsigned)((n + kMinWaves - 1) / kMinWaves)),
+                       dim3(64 * kMinWaves), 0, st, S, offsets, seg, lam, eps, E, C, K, M, W, m_star);
     return hipGetLastError();
 }
 

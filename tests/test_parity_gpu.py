@@ -84,6 +84,7 @@ RANDOM_CASES = [
     dict(seed=11, C=4, N=(256, 511, 512, 16385), L=3000, K=33, M=40, E=2),  # slice-floor sizes
     dict(seed=12, C=3, N=(300, 41, 2000), L=1500, K=77, M=3, E=8),         # 8 radii, 3 multipliers
     dict(seed=13, C=2, N=(500, 60), L=700, K=50, M=2, E=3),                 # 2 multipliers
+    dict(seed=14, C=3, N=(400, 90, 1200), L=900, K=21, M=300, E=70),       # 70 radii, 300 multipliers
 ]
 
 
