@@ -673,14 +673,14 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     if ((long long)p->S * B > 0x7fffffffLL || (long long)p->C > 0x7fffffffLL)
         return fail(ctx, DRO_ELIMIT, "S*B = %lld quantile blocks exceed 2^31 - 1", (long long)p->S * B);
     const size_t rows = (size_t)p->S * B;
-    rc = ensure_ws(ctx, rup(rows * kQWords * 4) + rup(rows * kQBuckets * 4), st);
+    rc = ensure_ws(ctx, rup(rows * kQStride * 4) + rup(rows * kQBuckets * 4), st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    uint32_t *fine = ar.take<uint32_t>(rows * kQWords);
+    uint32_t *fine = ar.take<uint32_t>(rows * kQStride);
     uint32_t *coarse = ar.take<uint32_t>(rows * kQBuckets);
     HIPCHK(launch_class_quantile(p->offsets, p->seg, p->xi, p->c_p, p->c_w, p->S, p->C, B, fine,
                                  coarse, q_value, q_rank, st));

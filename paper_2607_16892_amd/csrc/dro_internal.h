@@ -92,11 +92,12 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
 // ---- class_quantile (per-block packed histograms, then a select per class) ----
 constexpr int kQTop = 32768;              // largest sample value, 2^15
 constexpr int kQWords = kQTop / 2 + 1;    // packed 16-bit counts of the values 0 .. 2^15
+constexpr int kQStride = kQWords + 3;     // words per stored row and LDS copy (16-byte multiple)
 constexpr int kQBuckets = 256;            // coarse buckets of 128 values (the last also holds 2^15)
 constexpr long long kQMaxPart = 65535;    // samples per block, so every 16-bit count fits
 // blocks per segment: hist_parts, and enough that none holds more than kQMaxPart samples
 int qhist_parts(int S, long long max_seg, int num_cu);
-// fine: [S][B][kQWords] u32, coarse: [S][B][kQBuckets] u32 (scratch, fully written)
+// fine: [S][B][kQStride] u32, coarse: [S][B][kQBuckets] u32 (scratch, fully written)
 hipError_t launch_class_quantile(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
                                  const float *c_p, const float *c_w, int S, int C, int B,
                                  uint32_t *fine, uint32_t *coarse, int32_t *q_value,

@@ -71,15 +71,17 @@ hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 // 16-byte loads in flight, in two register sets of four: the next round's
 // loads are issued before this round's samples are counted.  Body vector i
 // goes to thread i mod kThreadsT, so even and odd threads see alternate
-// vectors.
-template <int kThreadsT, class F>
-__device__ __forceinline__ void for_each_sample(const int32_t *xi, long long lo, long long hi, F &&count)
+// vectors.  prologue() (block-wide: every thread calls it) runs once the
+// first four loads are in flight and before any count, so the block's set-up
+// (clearing its LDS counts) overlaps their latency.
+template <int kThreadsT, class F, class G>
+__device__ __forceinline__ void for_each_sample(const int32_t *xi, long long lo, long long hi, F &&count,
+                                                G &&prologue)
 {
     const int t = threadIdx.x;
     const long long mis = (long long)((reinterpret_cast<uintptr_t>(xi + lo) >> 2) & 3u);
     const long long a0 = min(hi, lo + ((4 - mis) & 3));
     const long long a1 = a0 + ((hi - a0) & ~3LL);
-    for (long long n = lo + t; n < a0; n += kThreadsT) count(xi[n]);
     const int4 *v4 = reinterpret_cast<const int4 *>(xi + a0);
     const long long nv = (a1 - a0) / 4;
     constexpr long long kRound = 4LL * kThreadsT;
@@ -104,6 +106,8 @@ __device__ __forceinline__ void for_each_sample(const int32_t *xi, long long lo,
         }
     };
     if (nv > 0) load(0, qa);
+    prologue();
+    for (long long n = lo + t; n < a0; n += kThreadsT) count(xi[n]);
     for (long long r0 = 0; r0 < nv; r0 += 2 * kRound) {
         load(r0 + kRound, qb);
         tally(r0, qa);
@@ -131,12 +135,16 @@ __global__ __launch_bounds__(kHistThreads) void histogram_kernel(const int64_t *
     const long long n0 = offsets[s], N = offsets[s + 1] - n0;
     const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
     const int t = threadIdx.x;
-    for (int i = t; i < kHistBins; i += kHistThreads) h[i] = 0;
-    __syncthreads();
-    for_each_sample<kHistThreads>(xi, lo, hi, [&](int v) {
-        v = v < 0 ? 0 : (v > kHistBins - 1 ? kHistBins - 1 : v);
-        atomicAdd(&h[v], 1u);
-    });
+    for_each_sample<kHistThreads>(
+        xi, lo, hi,
+        [&](int v) {
+            v = v < 0 ? 0 : (v > kHistBins - 1 ? kHistBins - 1 : v);
+            atomicAdd(&h[v], 1u);
+        },
+        [&] {
+            for (int i = t; i < kHistBins; i += kHistThreads) h[i] = 0;
+            __syncthreads();
+        });
     __syncthreads();
     uint32_t *o = hist + (long long)s * kHistBins;
     if (B == 1) {
@@ -158,56 +166,62 @@ __device__ int64_t exact_rank(float cp, float cw, int64_t N);
 // v mod 2^14, low half for v < 2^14, high half above; 2^15 in the low half of
 // word 2^14), in two copies: even threads add into one, odd threads into the
 // other, which halves the lanes of one wave that meet on one LDS word when
-// short lengths repeat.  It then stores, with plain stores, the two copies'
-// sum (every count fits 16 bits, as the block holds at most 65,535 samples)
-// and its counts per coarse bucket of 128 values.  No global atomics: the
-// select reads the B rows of the bucket it needs.
+// short lengths repeat.  It then stores, with plain 16-byte stores, the two
+// copies' sum (every count fits 16 bits, as the block holds at most 65,535
+// samples) and, in the same pass, its counts per coarse bucket of 128 values.
+// No global atomics: the select reads the B rows of the bucket it needs.
 constexpr int kQThreads = 1024;
 
 __global__ __launch_bounds__(kQThreads) void qhist_kernel(const int64_t *offsets, const int32_t *xi,
                                                           int B, uint32_t *fine, uint32_t *coarse)
 {
-    extern __shared__ uint32_t h[];  // 2 x kQWords words
+    extern __shared__ uint32_t h[];  // 2 x kQStride words
     const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
     const long long n0 = offsets[s], N = offsets[s + 1] - n0;
     const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
     const int t = threadIdx.x;
-    for (int i = t; i < 2 * kQWords; i += kQThreads) h[i] = 0;
+    uint32_t *hc = h + (t & 1) * kQStride;
+    uint4 *h4 = reinterpret_cast<uint4 *>(h);
+    const uint4 *g4 = reinterpret_cast<const uint4 *>(h + kQStride);
+    for_each_sample<kQThreads>(
+        xi, lo, hi,
+        [&](int v) {
+            v = v < 0 ? 0 : (v > kQTop ? kQTop : v);
+            // bit 14 of v selects the half (v = 2^15 has it clear)
+            atomicAdd(&hc[v < kQTop ? (v & (kQTop / 2 - 1)) : kQTop / 2], 1u << ((v >> 10) & 16));
+        },
+        [&] {
+            for (int i = t; i < 2 * kQStride / 4; i += kQThreads) h4[i] = make_uint4(0u, 0u, 0u, 0u);
+            __syncthreads();
+        });
     __syncthreads();
-    uint32_t *hc = h + (t & 1) * kQWords;
-    for_each_sample<kQThreads>(xi, lo, hi, [&](int v) {
-        v = v < 0 ? 0 : (v > kQTop ? kQTop : v);
-        // bit 14 of v selects the half (v = 2^15 has it clear)
-        atomicAdd(&hc[v < kQTop ? (v & (kQTop / 2 - 1)) : kQTop / 2], 1u << ((v >> 10) & 16));
-    });
-    __syncthreads();
-    uint32_t *out = fine + (long long)blockIdx.x * kQWords;
-    for (int w = t; w < kQWords; w += kQThreads) {
-        const uint32_t c = h[w] + h[kQWords + w];
-        h[w] = c;
-        out[w] = c;
-    }
-    __syncthreads();
-    // thread t: words [16 t, 16 t + 16), i.e. the values 16 t .. 16 t + 15
-    // (low halves, bucket t / 8) and 2^14 + 16 t .. (high halves, bucket
-    // 128 + t / 8); the reads start at a thread-dependent word to spread banks
-    static_assert(kQThreads * 16 == kQTop / 2, "one thread per 16 words");
-    uint32_t slo = 0, shi = 0;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const uint32_t c = h[16 * t + ((i + t) & 15)];
-        slo += c & 0xffffu;
-        shi += c >> 16;
-    }
-    for (int d = 1; d < 8; d <<= 1) {
-        slo += __shfl_xor(slo, d, 64);
-        shi += __shfl_xor(shi, d, 64);
-    }
+    // 16-byte word group q = t + 1024 i (i < 4) holds the words 4q .. 4q + 3:
+    // the values of coarse bucket q / 32 in its low halves and of bucket
+    // 128 + q / 32 in its high halves, so the 32 lanes t mod 32 = 0 .. 31 of a
+    // half-wave share both buckets.  The packed words add as plain 32-bit
+    // integers: no sum of low halves exceeds the block's 65,535 samples.
+    static_assert(kQThreads * 16 == kQTop / 2, "four word groups per thread");
+    static_assert(kQStride % 4 == 0 && kQStride >= kQTop / 2 + 4, "row of whole word groups");
+    uint4 *out = reinterpret_cast<uint4 *>(fine + (long long)blockIdx.x * kQStride);
     uint32_t *co = coarse + (long long)blockIdx.x * kQBuckets;
-    if ((t & 7) == 0) {
-        co[t >> 3] = slo;
-        // the last bucket also holds the value 2^15
-        co[128 + (t >> 3)] = shi + (t == kQThreads - 8 ? (h[kQTop / 2] & 0xffffu) : 0u);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = t + kQThreads * i;
+        const uint4 x = h4[q], y = g4[q];
+        const uint4 c = make_uint4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+        out[q] = c;
+        uint32_t p = (c.x + c.y) + (c.z + c.w);
+        for (int d = 1; d < 32; d <<= 1) p += __shfl_xor(p, d, 64);
+        if ((t & 31) == 0) {
+            const int bk = q >> 5;
+            co[bk] = p & 0xffffu;
+            // the last bucket also holds the value 2^15
+            co[128 + bk] = (p >> 16) + (bk == 127 ? (h[kQTop / 2] + h[kQStride + kQTop / 2]) & 0xffffu : 0u);
+        }
+    }
+    if (t == 0) {  // the group of the value 2^15 and the padding words
+        const uint4 x = h4[kQTop / 8], y = g4[kQTop / 8];
+        out[kQTop / 8] = make_uint4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
     }
 }
 
@@ -231,10 +245,11 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
     __shared__ long long sel_below;
     const int c = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int s = seg_of_x(seg, c);
-    const int64_t N = offsets[s + 1] - offsets[s];
-    const int64_t j = exact_rank(c_p[c], c_w[c], N);
+    // issued with the coarse loads below; the rank is formed once they are in flight
+    const int64_t o0 = offsets[s], o1 = offsets[s + 1];
+    const float cpc = c_p[c], cwc = c_w[c];
     const uint32_t *cs = coarse + (long long)s * B * kQBuckets;
-    const uint32_t *fs = fine + (long long)s * B * kQWords;
+    const uint32_t *fs = fine + (long long)s * B * kQStride;
     {
         const int q = t % kQBuckets, g = t / kQBuckets;
         uint32_t a = 0;
@@ -250,6 +265,7 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
         part[g][q] = a;
     }
     if (t == 0) sel = -1;
+    const int64_t j = exact_rank(cpc, cwc, o1 - o0);
     __syncthreads();
     // inclusive scan of the bucket totals (threads 0 .. 255), then the bucket
     // whose range of ranks holds j
@@ -287,16 +303,16 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
         uint32_t a = 0, a_top = 0;
         int bb = g;
         for (; bb + 3 * kFG < B; bb += 4 * kFG) {
-            const uint32_t x0 = fs[(long long)bb * kQWords + w];
-            const uint32_t x1 = fs[(long long)(bb + kFG) * kQWords + w];
-            const uint32_t x2 = fs[(long long)(bb + 2 * kFG) * kQWords + w];
-            const uint32_t x3 = fs[(long long)(bb + 3 * kFG) * kQWords + w];
+            const uint32_t x0 = fs[(long long)bb * kQStride + w];
+            const uint32_t x1 = fs[(long long)(bb + kFG) * kQStride + w];
+            const uint32_t x2 = fs[(long long)(bb + 2 * kFG) * kQStride + w];
+            const uint32_t x3 = fs[(long long)(bb + 3 * kFG) * kQStride + w];
             a += ((x0 >> sh) & 0xffffu) + ((x1 >> sh) & 0xffffu) + ((x2 >> sh) & 0xffffu) +
                  ((x3 >> sh) & 0xffffu);
         }
-        for (; bb < B; bb += kFG) a += (fs[(long long)bb * kQWords + w] >> sh) & 0xffffu;
+        for (; bb < B; bb += kFG) a += (fs[(long long)bb * kQStride + w] >> sh) & 0xffffu;
         if (top)
-            for (int r = g; r < B; r += kFG) a_top += fs[(long long)r * kQWords + kQTop / 2] & 0xffffu;
+            for (int r = g; r < B; r += kFG) a_top += fs[(long long)r * kQStride + kQTop / 2] & 0xffffu;
         fpart[g][o] = a;
         if (o == 0) fpart[g][128] = a_top;
     }
@@ -453,7 +469,7 @@ hipError_t qhist_prepare()
 {
     return hipFuncSetAttribute(reinterpret_cast<const void *>(qhist_kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                               (int)(2 * kQWords * sizeof(uint32_t)));
+                               (int)(2 * kQStride * sizeof(uint32_t)));
 }
 
 int qhist_parts(int S, long long max_seg, int num_cu)
@@ -468,7 +484,7 @@ hipError_t launch_class_quantile(const int64_t *offsets, const int32_t *seg, con
                                  int64_t *q_rank, hipStream_t st)
 {
     hipLaunchKernelGGL(qhist_kernel, dim3((unsigned)((long long)S * B)), dim3(kQThreads),
-                       2 * kQWords * sizeof(uint32_t), st, offsets, xi, B, fine, coarse);
+                       2 * kQStride * sizeof(uint32_t), st, offsets, xi, B, fine, coarse);
     HIPRET(hipGetLastError());
     hipLaunchKernelGGL(qselect_kernel, dim3((unsigned)C), dim3(kQThreads), 0, st, offsets, seg, c_p,
                        c_w, fine, coarse, B, q_value, q_rank);
