@@ -409,11 +409,17 @@ def main():
     ms_step = (t1 - t0) * 1e3 / max(args.steps, 1)
     launch_times = [e[1].elapsed_time(e[2]) for e in pairs]
     dense_ms = float(np.mean(launch_times))
-    breakdown = {"quantile_ms": float(np.median([e[0].elapsed_time(e[1]) for e in pairs])),
+    q_ms = float(np.median([e[0].elapsed_time(e[1]) for e in pairs]))
+    q_bytes = 4 * int(w.offsets[-1])  # the int32 samples, each read once
+    breakdown = {"quantile_ms": q_ms,
+                 "quantile_sample_bytes": q_bytes,
+                 "quantile_gbs": q_bytes / (q_ms * 1e-3) / 1e9,
                  "cost_eval_ms": float(np.median(launch_times)),
                  "argmin_ms": float(np.median([e[2].elapsed_time(e[3]) for e in pairs])),
                  "note": "HIP events on the launch stream around class_quantile, dro_cost_eval "
-                         "and dro_argmin_reservation; medians over the timed steps"}
+                         "and dro_argmin_reservation; medians over the timed steps; "
+                         "quantile_gbs = the samples' bytes over the whole call's time "
+                         "(both launches and the gaps between the events)"}
     evals = w.evals
     value = evals / (ms_step / 1e3)
     dense_rate = evals / (dense_ms / 1e3)

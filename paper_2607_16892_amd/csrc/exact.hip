@@ -243,11 +243,15 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
     __shared__ uint32_t wsum[kQBuckets / 64];
     __shared__ int sel;
     __shared__ long long sel_below;
+    __shared__ int64_t s_off[2], s_rank;
+    __shared__ float s_cost[2];
     const int c = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int s = seg_of_x(seg, c);
-    // issued with the coarse loads below; the rank is formed once they are in flight
-    const int64_t o0 = offsets[s], o1 = offsets[s + 1];
-    const float cpc = c_p[c], cwc = c_w[c];
+    // the rank's inputs, loaded by every thread from addresses that differ by
+    // lane: vector loads in flight with the coarse loads below, not waited for
+    // before them as uniform scalar loads would be
+    const int64_t r_off = offsets[s + (t & 1)];
+    const float r_cost = ((t & 2) ? c_w : c_p)[c];
     const uint32_t *cs = coarse + (long long)s * B * kQBuckets;
     const uint32_t *fs = fine + (long long)s * B * kQStride;
     {
@@ -265,8 +269,10 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
         part[g][q] = a;
     }
     if (t == 0) sel = -1;
-    const int64_t j = exact_rank(cpc, cwc, o1 - o0);
+    if (t < 2) s_off[t] = r_off;         // offsets[s], offsets[s + 1]
+    if ((t | 2) == 2) s_cost[t >> 1] = r_cost;  // t = 0: c_p[c], t = 2: c_w[c]
     __syncthreads();
+    if (t == 0) s_rank = exact_rank(s_cost[0], s_cost[1], s_off[1] - s_off[0]);
     // inclusive scan of the bucket totals (threads 0 .. 255), then the bucket
     // whose range of ranks holds j
     uint32_t tot = 0, incl = 0;
@@ -281,6 +287,7 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
         if (lane == 63) wsum[wave] = incl;
     }
     __syncthreads();
+    const int64_t j = s_rank;
     if (t < kQBuckets) {
         for (int w = 0; w < wave; ++w) incl += wsum[w];
         const int64_t before = (int64_t)(incl - tot);
