@@ -85,6 +85,7 @@ RANDOM_CASES = [
     dict(seed=12, C=3, N=(300, 41, 2000), L=1500, K=77, M=3, E=8),         # 8 radii, 3 multipliers
     dict(seed=13, C=2, N=(500, 60), L=700, K=50, M=2, E=3),                 # 2 multipliers
     dict(seed=14, C=3, N=(400, 90, 1200), L=900, K=21, M=300, E=70),       # 70 radii, 300 multipliers
+    dict(seed=15, C=2, N=(300, 50), L=500, K=17, M=9, E=1000),              # 1000 radii: 16 lane-group passes
 ]
 
 
