@@ -478,53 +478,55 @@ __global__ __launch_bounds__(64 * kMinWaves) void min_over_lambda_kernel(
 {
     __shared__ double2 st[kMinWaves][kMinChunk];  // (q_m, lambda_m)
     const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const long long ck = (long long)blockIdx.x * kMinWaves + w;
-    if (ck >= (long long)C * K) return;  // whole waves; no block barrier below
-    const int c = (int)(ck / K), k = (int)(ck % K);
-    const int s = seg_of(seg, c);
-    const double N = (double)(offsets[s + 1] - offsets[s]);
-    const double *row = S + ck * M;
-    int lg = 0;  // log2 of the groups
-    while (lg < 6 && (1 << lg) < E) ++lg;
-    const int lp = 6 - lg;  // log2 of the lanes per group
-    const int part = lane & ((1 << lp) - 1), grp = lane >> lp;
-    double2 *q = st[w];
-    for (int e0 = 0; e0 < E; e0 += 1 << lg) {
-        const int e = e0 + grp;
-        const double ev = e < E ? (double)eps[(long long)e * C + c] : 0.0;
-        double best = __builtin_inf();
-        int bm = M;  // no multiplier yet: loses every comparison below
-        for (int m0 = 0; m0 < M; m0 += kMinChunk) {
-            const int mc = min(kMinChunk, M - m0);
-            if (e0 == 0 || M > kMinChunk) {  // else the one chunk is still staged
-                __builtin_amdgcn_wave_barrier();  // the last chunk's reads come first
-                for (int i = lane; i < mc; i += 64)
-                    q[i] = make_double2(__ddiv_rn(row[m0 + i], N), (double)lam[m0 + i]);
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            }
-            for (int i = part; i < mc; i += 1 << lp) {
-                const double2 v = q[i];
-                const double J = __dadd_rn(__dmul_rn(v.y, ev), v.x);
-                if (J < best) {
-                    best = J;
-                    bm = m0 + i;
+    // rows in a grid-stride loop of whole waves (no block barrier below)
+    for (long long ck = (long long)blockIdx.x * kMinWaves + w; ck < (long long)C * K;
+         ck += (long long)gridDim.x * kMinWaves) {
+        const int c = (int)(ck / K), k = (int)(ck % K);
+        const int s = seg_of(seg, c);
+        const double N = (double)(offsets[s + 1] - offsets[s]);
+        const double *row = S + ck * M;
+        int lg = 0;  // log2 of the groups
+        while (lg < 6 && (1 << lg) < E) ++lg;
+        const int lp = 6 - lg;  // log2 of the lanes per group
+        const int part = lane & ((1 << lp) - 1), grp = lane >> lp;
+        double2 *q = st[w];
+        for (int e0 = 0; e0 < E; e0 += 1 << lg) {
+            const int e = e0 + grp;
+            const double ev = e < E ? (double)eps[(long long)e * C + c] : 0.0;
+            double best = __builtin_inf();
+            int bm = M;  // no multiplier yet: loses every comparison below
+            for (int m0 = 0; m0 < M; m0 += kMinChunk) {
+                const int mc = min(kMinChunk, M - m0);
+                if (e0 == 0 || M > kMinChunk) {  // else the one chunk is still staged
+                    __builtin_amdgcn_wave_barrier();  // the last chunk's reads come first
+                    for (int i = lane; i < mc; i += 64)
+                        q[i] = make_double2(__ddiv_rn(row[m0 + i], N), (double)lam[m0 + i]);
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                }
+                for (int i = part; i < mc; i += 1 << lp) {
+                    const double2 v = q[i];
+                    const double J = __dadd_rn(__dmul_rn(v.y, ev), v.x);
+                    if (J < best) {
+                        best = J;
+                        bm = m0 + i;
+                    }
                 }
             }
-        }
-        for (int d = (1 << lp) >> 1; d >= 1; d >>= 1) {
-            const double ob = __shfl_xor(best, d, 64);
-            const int om = __shfl_xor(bm, d, 64);
-            if (ob < best || (ob == best && om < bm)) {
-                best = ob;
-                bm = om;
+            for (int d = (1 << lp) >> 1; d >= 1; d >>= 1) {
+                const double ob = __shfl_xor(best, d, 64);
+                const int om = __shfl_xor(bm, d, 64);
+                if (ob < best || (ob == best && om < bm)) {
+                    best = ob;
+                    bm = om;
+                }
             }
-        }
-        if (part == 0 && e < E) {
-            const long long o = ((long long)e * C + c) * K + k;
-            W[o] = best;
-            if (m_star) m_star[o] = bm;
+            if (part == 0 && e < E) {
+                const long long o = ((long long)e * C + c) * K + k;
+                W[o] = best;
+                if (m_star) m_star[o] = bm;
+            }
         }
     }
 }
@@ -534,7 +536,9 @@ hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const
                                   double *W, int32_t *m_star, hipStream_t st)
 {
     const long long n = (long long)C * K;
-    hipLaunchKernelGGL(min_over_lambda_kernel, dim3((unsigned)((n + kMinWaves - 1) / kMinWaves)),
+    // at most 2^20 blocks: the grid's work-item count stays below 2^32
+    const long long blocks = std::min((n + kMinWaves - 1) / kMinWaves, 1LL << 20);
+    hipLaunchKernelGGL(min_over_lambda_kernel, dim3((unsigned)blocks),
                        dim3(64 * kMinWaves), 0, st, S, offsets, seg, lam, eps, E, C, K, M, W, m_star);
     return hipGetLastError();
 }

@@ -842,91 +842,84 @@ hipError_t launch_prefix(const uint32_t *hist, int S, uint32_t *cnt, uint64_t *s
     return hipGetLastError();
 }
 
-// Block per (class, KB = 256 / TM consecutive grid points), TM threads per
-// grid point (TM = the power of two >= min(M, 256)), each taking the
-// multipliers m = ml, ml + TM, ...: exact S, exact J for every radius row, and
-// per grid point the minimum over m with the lowest m (W, m_star), radius rows
-// in groups of 8 reduced over each grid point's TM threads in LDS.  The lowest
-// (J, m) does not depend on the order of the reduction.
-constexpr int kTableThreads = 256;
+// One wave per (c, k) row, as the minimum over the multipliers of the dense
+// path: the wave computes each multiplier's exact S from the segment's prefix
+// counts and sums once and stages q_m = RN(S / N) with lambda_m in LDS, a
+// chunk of multipliers at a time; then its 64 lanes split into g groups of
+// 64/g, g the power of two covering E (at most 64), group j taking radius
+// e0 + j and its lanes the multipliers m = part, part + 64/g, ... of the
+// chunk.  Each lane keeps the smallest J of its multipliers (the lowest m among
+// equal values, as it visits them in ascending order), and log2(64/g) shuffle
+// steps take the group's smallest J, ties to the lowest m (W, m_star): the
+// same values and the same lowest m as a scan over m.
+constexpr int kTableWaves = 4;    // waves (rows) per block
+constexpr int kTableChunk = 256;  // multipliers staged per wave at a time
 
-template <int TM>
-__global__ __launch_bounds__(kTableThreads) void exact_table_kernel(
+__global__ __launch_bounds__(64 * kTableWaves) void exact_table_kernel(
     const int64_t *offsets, const int32_t *seg, const int32_t *L_, const int32_t *eta_,
     const float *lam, const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt,
     const uint64_t *sum, int E, int C, int K, int M, double *W, int32_t *m_star)
 {
-    __shared__ double rv[8][kTableThreads];
-    __shared__ int rm[8][kTableThreads];
-    const int KB = kTableThreads / TM;
-    const int kgroups = (K + KB - 1) / KB;
-    const int c = (int)(blockIdx.x / kgroups);
-    const int t = threadIdx.x, ml = t % TM;
-    const int k = (int)(blockIdx.x % kgroups) * KB + t / TM;
-    const int s = seg_of_x(seg, c);
-    const int64_t N = offsets[s + 1] - offsets[s];
-    const int64_t L = L_[c], eta = eta_[k < K ? k : K - 1];
-    const uint32_t *cn = cnt + (long long)s * kHistBins;
-    const uint64_t *sm = sum + (long long)s * kHistBins;
-    const int64_t CP = fix33(c_p[c]), CW = fix33(c_w[c]);
-    const double Nd = (double)N;
-    for (int e0 = 0; e0 < E; e0 += 8) {
-        double best[8];
-        int bm[8];
-        double ev[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            best[q] = __builtin_inf();
-            bm[q] = 0x7fffffff;
-            ev[q] = (e0 + q < E) ? (double)eps[(long long)(e0 + q) * C + c] : 0.0;
-        }
-        for (int m = ml; m < M; m += TM) {
-            const unsigned __int128 u = exact_S_prefix(cn, sm, N, L, eta, CP, CW, fix33(lam[m]));
-            const double q_ = __ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), Nd);
-            const double lm = (double)lam[m];
-            const int nq = E - e0;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                if (q >= nq) break;
-                const double J = __dadd_rn(__dmul_rn(lm, ev[q]), q_);
-                if (J < best[q]) {  // m ascending: the first minimiser of this thread
-                    best[q] = J;
-                    bm[q] = m;
+    __shared__ double2 stq[kTableWaves][kTableChunk];  // (q_m, lambda_m)
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    // rows in a grid-stride loop of whole waves (no block barrier below)
+    for (long long ck = (long long)blockIdx.x * kTableWaves + wv; ck < (long long)C * K;
+         ck += (long long)gridDim.x * kTableWaves) {
+        const int c = (int)(ck / K), k = (int)(ck % K);
+        const int s = seg_of_x(seg, c);
+        const int64_t N = offsets[s + 1] - offsets[s];
+        const int64_t L = L_[c], eta = eta_[k];
+        const uint32_t *cn = cnt + (long long)s * kHistBins;
+        const uint64_t *sm = sum + (long long)s * kHistBins;
+        const int64_t CP = fix33(c_p[c]), CW = fix33(c_w[c]);
+        const double Nd = (double)N;
+        int lg = 0;  // log2 of the groups
+        while (lg < 6 && (1 << lg) < E) ++lg;
+        const int lp = 6 - lg;  // log2 of the lanes per group
+        const int part = lane & ((1 << lp) - 1), grp = lane >> lp;
+        double2 *q = stq[wv];
+        for (int e0 = 0; e0 < E; e0 += 1 << lg) {
+            const int e = e0 + grp;
+            const double ev = e < E ? (double)eps[(long long)e * C + c] : 0.0;
+            double best = __builtin_inf();
+            int bm = M;  // no multiplier yet: loses every comparison below
+            for (int m0 = 0; m0 < M; m0 += kTableChunk) {
+                const int mc = min(kTableChunk, M - m0);
+                if (e0 == 0 || M > kTableChunk) {  // else the one chunk is still staged
+                    __builtin_amdgcn_wave_barrier();  // the last chunk's reads come first
+                    for (int i = lane; i < mc; i += 64) {
+                        const float lm = lam[m0 + i];
+                        const unsigned __int128 u = exact_S_prefix(cn, sm, N, L, eta, CP, CW, fix33(lm));
+                        q[i] = make_double2(__ddiv_rn(fix128_to_double((uint64_t)u, (uint64_t)(u >> 64)), Nd),
+                                            (double)lm);
+                    }
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    __builtin_amdgcn_wave_barrier();
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
                 }
-            }
-        }
-        const int nq = E - e0 < 8 ? E - e0 : 8;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            rv[q][t] = best[q];
-            rm[q][t] = bm[q];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int w = TM / 2; w > 0; w >>= 1) {  // within each grid point's TM threads
-            if (ml < w) {
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    if (q >= nq) break;
-                    const double v2 = rv[q][t + w];
-                    const int m2 = rm[q][t + w];
-                    if (v2 < rv[q][t] || (v2 == rv[q][t] && m2 < rm[q][t])) {
-                        rv[q][t] = v2;
-                        rm[q][t] = m2;
+                for (int i = part; i < mc; i += 1 << lp) {
+                    const double2 v = q[i];
+                    const double J = __dadd_rn(__dmul_rn(v.y, ev), v.x);
+                    if (J < best) {
+                        best = J;
+                        bm = m0 + i;
                     }
                 }
             }
-            __syncthreads();
-        }
-        if (k < K) {  // the grid point's threads write its rows, thread ml rows ml, ml + TM, ...
-            const int g0 = t - ml;
-            for (int q = ml; q < nq; q += TM) {
-                const long long o = ((long long)(e0 + q) * C + c) * K + k;
-                W[o] = rv[q][g0];
-                m_star[o] = rm[q][g0];
+            for (int d = (1 << lp) >> 1; d >= 1; d >>= 1) {
+                const double ob = __shfl_xor(best, d, 64);
+                const int om = __shfl_xor(bm, d, 64);
+                if (ob < best || (ob == best && om < bm)) {
+                    best = ob;
+                    bm = om;
+                }
+            }
+            if (part == 0 && e < E) {
+                const long long o = ((long long)e * C + c) * K + k;
+                W[o] = best;
+                m_star[o] = bm;
             }
         }
-        __syncthreads();
     }
 }
 
@@ -991,28 +984,12 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
                               int32_t *k_star, double *W_star, int32_t *m_at_star, hipStream_t st)
 {
     HIPRET(launch_prefix(hist, S, cnt, sum, st));
-    int TM = 1;  // threads per grid point
-    while (TM < M && TM < kTableThreads) TM *= 2;
-    const int KB = kTableThreads / TM;
-    const long long n = (long long)C * ((K + KB - 1) / KB);
-#define DRO_TABLE_CASE(tm)                                                                        \
-    case tm:                                                                                      \
-        hipLaunchKernelGGL(exact_table_kernel<tm>, dim3((unsigned)n), dim3(kTableThreads), 0, st, \
-                           offsets, seg, L, eta, lam, c_p, c_w, eps, (const uint32_t *)cnt,       \
-                           (const uint64_t *)sum, E, C, K, M, W, m_star);                        \
-        break;
-    switch (TM) {
-        DRO_TABLE_CASE(1)
-        DRO_TABLE_CASE(2)
-        DRO_TABLE_CASE(4)
-        DRO_TABLE_CASE(8)
-        DRO_TABLE_CASE(16)
-        DRO_TABLE_CASE(32)
-        DRO_TABLE_CASE(64)
-        DRO_TABLE_CASE(128)
-        DRO_TABLE_CASE(256)
-    }
-#undef DRO_TABLE_CASE
+    const long long rows = (long long)C * K;
+    // at most 2^20 blocks: the grid's work-item count stays below 2^32
+    const long long blocks = std::min((rows + kTableWaves - 1) / kTableWaves, 1LL << 20);
+    hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)blocks),
+                       dim3(64 * kTableWaves), 0, st, offsets, seg, L, eta, lam, c_p, c_w, eps,
+                       (const uint32_t *)cnt, (const uint64_t *)sum, E, C, K, M, W, m_star);
     if (k_star) HIPRET(launch_table_argmin(W, m_star, k_max, E, C, K, k_star, W_star, m_at_star, st));
     return hipGetLastError();
 }
