@@ -32,6 +32,8 @@ struct dro_ctx {
     // the next configuration search on this context has been enqueued)
     std::vector<long long> ways_h;
     std::vector<int32_t> gpus_h;
+    // host copy of the quantile's row table (segments with unequal part counts)
+    std::vector<int64_t> qboff_h;
 };
 
 // Scratch of dro_cost_eval_noalloc: a fixed array in every device's memory,
@@ -669,21 +671,42 @@ int class_quantile(dro_ctx *ctx, const dro_problem *p, int32_t *q_value, int64_t
     if (!q_value || !q_rank) return fail(ctx, DRO_EINVAL, "q_value and q_rank must be non-NULL");
     ENTER_DEVICE(ctx);
     hipStream_t st = (hipStream_t)stream;
-    const int B = qhist_parts(p->S, sh.max_n, ctx->num_cu);
-    if ((long long)p->S * B > 0x7fffffffLL || (long long)p->C > 0x7fffffffLL)
-        return fail(ctx, DRO_ELIMIT, "S*B = %lld quantile blocks exceed 2^31 - 1", (long long)p->S * B);
-    const size_t rows = (size_t)p->S * B;
-    rc = ensure_ws(ctx, rup(rows * kQStride * 4) + rup(rows * kQBuckets * 4), st);
+    // parts per segment (one row of counts each); one count for all segments
+    // when they agree, else a row table: segment s owns rows boff[s] .. boff[s+1]
+    const int64_t *o = p->offsets_h;
+    long long B = 0, rows = 0;
+    bool uniform = true;
+    for (int s = 0; s < p->S; ++s) {
+        const long long b = qhist_parts(p->S, o[s + 1] - o[s], ctx->num_cu);
+        if (s == 0) B = b;
+        else if (b != B) uniform = false;
+        rows += b;
+    }
+    if (rows > 0x7fffffffLL)
+        return fail(ctx, DRO_ELIMIT, "%lld quantile rows exceed 2^31 - 1", rows);
+    std::vector<int64_t> &bo = ctx->qboff_h;
+    if (!uniform) {
+        bo.assign((size_t)p->S + 1, 0);
+        for (int s = 0; s < p->S; ++s) bo[s + 1] = bo[s] + qhist_parts(p->S, o[s + 1] - o[s], ctx->num_cu);
+    }
+    const size_t table = uniform ? 0 : rup(((size_t)p->S + 1) * 8);
+    rc = ensure_ws(ctx, rup((size_t)rows * kQStride * 4) + rup((size_t)rows * kQBuckets * 4) + table, st);
     if (rc) return rc;
     Arena ar{(char *)ctx->ws, 0};
     dro_problem q;
     rc = stage_problem(ctx, p, ar, st, &q);
     if (rc) return rc;
     p = &q;
-    uint32_t *fine = ar.take<uint32_t>(rows * kQStride);
-    uint32_t *coarse = ar.take<uint32_t>(rows * kQBuckets);
-    HIPCHK(launch_class_quantile(p->offsets, p->seg, p->xi, p->c_p, p->c_w, p->S, p->C, B, fine,
-                                 coarse, q_value, q_rank, st));
+    uint32_t *fine = ar.take<uint32_t>((size_t)rows * kQStride);
+    uint32_t *coarse = ar.take<uint32_t>((size_t)rows * kQBuckets);
+    int64_t *boff = nullptr;
+    if (!uniform) {  // pageable source: copied out before the call returns
+        boff = ar.take<int64_t>((size_t)p->S + 1);
+        HIPCHK(hipMemcpyAsync(boff, bo.data(), ((size_t)p->S + 1) * 8, hipMemcpyHostToDevice, st));
+    }
+    HIPCHK(launch_class_quantile(p->offsets, p->seg, p->xi, p->c_p, p->c_w, p->S, p->C,
+                                 uniform ? (int)B : 0, boff, rows, fine, coarse, q_value, q_rank,
+                                 st));
     return DRO_OK;
 }
 

@@ -390,9 +390,12 @@ hipError_t launch_dense(const DenseArgs &a, hipStream_t st)
 
 __global__ void zero_u64_u32_kernel(unsigned long long *p, long long n, uint32_t *q, long long nq)
 {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0ull;
-    if (i < nq) q[i] = 0u;
+    const long long m = n > nq ? n : nq;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < m;
+         i += (long long)gridDim.x * blockDim.x) {
+        if (i < n) p[i] = 0ull;
+        if (i < nq) q[i] = 0u;
+    }
 }
 
 hipError_t launch_zero_u64_u32(unsigned long long *p, long long n, uint32_t *q, long long nq,
@@ -400,8 +403,8 @@ hipError_t launch_zero_u64_u32(unsigned long long *p, long long n, uint32_t *q, 
 {
     const long long m = std::max(n, nq);
     if (m <= 0) return hipSuccess;
-    hipLaunchKernelGGL(zero_u64_u32_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, st, p,
-                       n, q, nq);
+    hipLaunchKernelGGL(zero_u64_u32_kernel, dim3((unsigned)std::min((m + 255) / 256, kMaxGridBlocks)),
+                       dim3(256), 0, st, p, n, q, nq);
     return hipGetLastError();
 }
 
@@ -416,11 +419,9 @@ __device__ __forceinline__ long long count_le(const uint32_t *cn, long long v, l
 // S[c,k,m] from the per-sample sums sum |x - t_c| of the dense kernel (in R,
 // overwritten in place), the segment's value counts and its sample sum:
 // exactly, in 128-bit integers in units of 2^-33, then rounded to double once.
-__global__ void dense_finish_kernel(DenseFinishArgs a)
+__device__ __forceinline__ void dense_finish_one(const DenseFinishArgs &a, long long i)
 {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     const long long KM = (long long)a.K * a.M;
-    if (i >= (long long)a.C * KM) return;
     const int c = (int)(i / KM);
     const int k = (int)((i / a.M) % a.K);
     const int m = (int)(i % a.M);
@@ -453,10 +454,19 @@ __global__ void dense_finish_kernel(DenseFinishArgs a)
     reinterpret_cast<double *>(a.R)[i] = sfix128_to_double(S);
 }
 
+__global__ void dense_finish_kernel(DenseFinishArgs a)
+{
+    const long long n = (long long)a.C * a.K * a.M;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (long long)gridDim.x * blockDim.x)
+        dense_finish_one(a, i);
+}
+
 hipError_t launch_dense_finish(const DenseFinishArgs &a, hipStream_t st)
 {
     const long long n = (long long)a.C * a.K * a.M;
-    hipLaunchKernelGGL(dense_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(dense_finish_kernel, dim3((unsigned)std::min((n + 255) / 256, kMaxGridBlocks)),
+                       dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
@@ -536,8 +546,7 @@ hipError_t launch_min_over_lambda(const double *S, const int64_t *offsets, const
                                   double *W, int32_t *m_star, hipStream_t st)
 {
     const long long n = (long long)C * K;
-    // at most 2^20 blocks: the grid's work-item count stays below 2^32
-    const long long blocks = std::min((n + kMinWaves - 1) / kMinWaves, 1LL << 20);
+    const long long blocks = std::min((n + kMinWaves - 1) / kMinWaves, kMaxGridBlocks);
     hipLaunchKernelGGL(min_over_lambda_kernel, dim3((unsigned)blocks),
                        dim3(64 * kMinWaves), 0, st, S, offsets, seg, lam, eps, E, C, K, M, W, m_star);
     return hipGetLastError();

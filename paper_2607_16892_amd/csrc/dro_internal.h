@@ -50,6 +50,11 @@ struct DenseArgs {
 hipError_t launch_dense(const DenseArgs &a, hipStream_t st);
 // resident dense blocks per compute unit (occupancy of dense_kernel)
 int dense_blocks_per_cu();
+// Launches whose block count grows with the problem loop over their items or
+// rows with at most kMaxGridBlocks blocks, so a grid stays below 2^32
+// work-items whatever the sizes.
+constexpr long long kMaxGridBlocks = 1LL << 20;
+
 // zeroes p[0, n) and q[0, nq)
 hipError_t launch_zero_u64_u32(unsigned long long *p, long long n, uint32_t *q, long long nq,
                                hipStream_t st);
@@ -95,13 +100,17 @@ constexpr int kQWords = kQTop / 2 + 1;    // packed 16-bit counts of the values 
 constexpr int kQStride = kQWords + 3;     // words per stored row and LDS copy (16-byte multiple)
 constexpr int kQBuckets = 256;            // coarse buckets of 128 values (the last also holds 2^15)
 constexpr long long kQMaxPart = 65535;    // samples per block, so every 16-bit count fits
-// blocks per segment: hist_parts, and enough that none holds more than kQMaxPart samples
-int qhist_parts(int S, long long max_seg, int num_cu);
+// blocks (parts) of a segment of n samples: about one block per compute unit
+// over all S segments, each holding at most kQMaxPart samples
+long long qhist_parts(int S, long long n, int num_cu);
 // fine: [S][B][kQStride] u32, coarse: [S][B][kQBuckets] u32 (scratch, fully written)
+// Parts: B per segment when boff is null (rows = S B), else boff[s] .. boff[s+1]
+// are segment s's rows (device int64 [S+1], rows = boff[S]).
 hipError_t launch_class_quantile(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
                                  const float *c_p, const float *c_w, int S, int C, int B,
-                                 uint32_t *fine, uint32_t *coarse, int32_t *q_value,
-                                 int64_t *q_rank, hipStream_t st);
+                                 const int64_t *boff, long long rows, uint32_t *fine,
+                                 uint32_t *coarse, int32_t *q_value, int64_t *q_rank,
+                                 hipStream_t st);
 
 // ---- exact table (value counts and prefix sums) -------------------------------
 // The prefix pass works in chunks of 4096 bins.  A sum array holds the S x

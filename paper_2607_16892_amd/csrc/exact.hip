@@ -53,15 +53,17 @@ __device__ __forceinline__ unsigned __int128 exact_S_prefix(const uint32_t *cn, 
 
 __global__ void fill_u32_kernel(uint32_t *p, long long n, uint32_t v)
 {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = v;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (long long)gridDim.x * blockDim.x)
+        p[i] = v;
 }
 
 // -------------------------------------------------------------- quantile ----
 hipError_t launch_fill_u32(uint32_t *p, long long n, uint32_t v, hipStream_t st)
 {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n, v);
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)std::min((n + 255) / 256, kMaxGridBlocks)),
+                       dim3(256), 0, st, p, n, v);
     return hipGetLastError();
 }
 
@@ -161,7 +163,8 @@ __device__ int64_t exact_rank(float cp, float cw, int64_t N);
 
 // ---- class_quantile: per-block histograms, then one select per class ----
 //
-// Block (segment s, part b of B, at most kQMaxPart samples) counts its share
+// Block for row r (segment s, part b of its B_s parts, at most kQMaxPart
+// samples; rows in a block-uniform loop) counts its share
 // in LDS with 16-bit counts packed two to a word (value v < 2^15 in word
 // v mod 2^14, low half for v < 2^14, high half above; 2^15 in the low half of
 // word 2^14), in two copies: even threads add into one, odd threads into the
@@ -176,55 +179,76 @@ constexpr int kQThreads = 1024;
 typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kQThreads) void qhist_kernel(const int64_t *offsets, const int32_t *xi,
-                                                          int B, uint32_t *fine, uint32_t *coarse)
+                                                          int S, int B, const int64_t *boff,
+                                                          long long rows, uint32_t *fine,
+                                                          uint32_t *coarse)
 {
     extern __shared__ uint32_t h[];  // 2 x kQStride words
-    const int s = (int)(blockIdx.x / B), b = (int)(blockIdx.x % B);
-    const long long n0 = offsets[s], N = offsets[s + 1] - n0;
-    const long long lo = n0 + (N * b) / B, hi = n0 + (N * (b + 1)) / B;
     const int t = threadIdx.x;
-    uint32_t *hc = h + (t & 1) * kQStride;
-    uint4 *h4 = reinterpret_cast<uint4 *>(h);
-    const uint4 *g4 = reinterpret_cast<const uint4 *>(h + kQStride);
-    for_each_sample<kQThreads>(
-        xi, lo, hi,
-        [&](int v) {
-            v = v < 0 ? 0 : (v > kQTop ? kQTop : v);
-            // bit 14 of v selects the half (v = 2^15 has it clear)
-            atomicAdd(&hc[v < kQTop ? (v & (kQTop / 2 - 1)) : kQTop / 2], 1u << ((v >> 10) & 16));
-        },
-        [&] {
-            for (int i = t; i < 2 * kQStride / 4; i += kQThreads) h4[i] = make_uint4(0u, 0u, 0u, 0u);
-            __syncthreads();
-        });
-    __syncthreads();
-    // 16-byte word group q = t + 1024 i (i < 4) holds the words 4q .. 4q + 3:
-    // the values of coarse bucket q / 32 in its low halves and of bucket
-    // 128 + q / 32 in its high halves, so the 32 lanes t mod 32 = 0 .. 31 of a
-    // half-wave share both buckets.  The packed words add as plain 32-bit
-    // integers: no sum of low halves exceeds the block's 65,535 samples.
-    static_assert(kQThreads * 16 == kQTop / 2, "four word groups per thread");
-    static_assert(kQStride % 4 == 0 && kQStride >= kQTop / 2 + 4, "row of whole word groups");
-    uint4 *out = reinterpret_cast<uint4 *>(fine + (long long)blockIdx.x * kQStride);
-    uint32_t *co = coarse + (long long)blockIdx.x * kQBuckets;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int q = t + kQThreads * i;
-        const uint4 x = h4[q], y = g4[q];
-        const uint4 c = make_uint4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
-        __builtin_nontemporal_store(u32x4_nt{c.x, c.y, c.z, c.w}, reinterpret_cast<u32x4_nt *>(out + q));
-        uint32_t p = (c.x + c.y) + (c.z + c.w);
-        for (int d = 1; d < 32; d <<= 1) p += __shfl_xor(p, d, 64);
-        if ((t & 31) == 0) {
-            const int bk = q >> 5;
-            co[bk] = p & 0xffffu;
-            // the last bucket also holds the value 2^15
-            co[128 + bk] = (p >> 16) + (bk == 127 ? (h[kQTop / 2] + h[kQStride + kQTop / 2]) & 0xffffu : 0u);
+    for (long long r = blockIdx.x; r < rows; r += gridDim.x) {
+        int s;
+        long long b, Bs;
+        if (boff) {  // the segment whose rows hold r: boff[s] <= r < boff[s + 1]
+            int a = 0, z = S;
+            while (z - a > 1) {
+                const int mid = (a + z) >> 1;
+                if (boff[mid] <= r) a = mid;
+                else z = mid;
+            }
+            s = a;
+            b = r - boff[s];
+            Bs = boff[s + 1] - boff[s];
+        } else {
+            s = (int)(r / B);
+            b = r % B;
+            Bs = B;
         }
-    }
-    if (t == 0) {  // the group of the value 2^15 and the padding words
-        const uint4 x = h4[kQTop / 8], y = g4[kQTop / 8];
-        out[kQTop / 8] = make_uint4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+        const long long n0 = offsets[s], N = offsets[s + 1] - n0;
+        const long long lo = n0 + (N * b) / Bs, hi = n0 + (N * (b + 1)) / Bs;
+        uint32_t *hc = h + (t & 1) * kQStride;
+        uint4 *h4 = reinterpret_cast<uint4 *>(h);
+        const uint4 *g4 = reinterpret_cast<const uint4 *>(h + kQStride);
+        for_each_sample<kQThreads>(
+            xi, lo, hi,
+            [&](int v) {
+                v = v < 0 ? 0 : (v > kQTop ? kQTop : v);
+                // bit 14 of v selects the half (v = 2^15 has it clear)
+                atomicAdd(&hc[v < kQTop ? (v & (kQTop / 2 - 1)) : kQTop / 2], 1u << ((v >> 10) & 16));
+            },
+            [&] {
+                for (int i = t; i < 2 * kQStride / 4; i += kQThreads) h4[i] = make_uint4(0u, 0u, 0u, 0u);
+                __syncthreads();
+            });
+        __syncthreads();
+        // 16-byte word group q = t + 1024 i (i < 4) holds the words 4q .. 4q + 3:
+        // the values of coarse bucket q / 32 in its low halves and of bucket
+        // 128 + q / 32 in its high halves, so the 32 lanes t mod 32 = 0 .. 31 of a
+        // half-wave share both buckets.  The packed words add as plain 32-bit
+        // integers: no sum of low halves exceeds the block's 65,535 samples.
+        static_assert(kQThreads * 16 == kQTop / 2, "four word groups per thread");
+        static_assert(kQStride % 4 == 0 && kQStride >= kQTop / 2 + 4, "row of whole word groups");
+        uint4 *out = reinterpret_cast<uint4 *>(fine + r * kQStride);
+        uint32_t *co = coarse + r * kQBuckets;
+    #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = t + kQThreads * i;
+            const uint4 x = h4[q], y = g4[q];
+            const uint4 c = make_uint4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+            __builtin_nontemporal_store(u32x4_nt{c.x, c.y, c.z, c.w}, reinterpret_cast<u32x4_nt *>(out + q));
+            uint32_t p = (c.x + c.y) + (c.z + c.w);
+            for (int d = 1; d < 32; d <<= 1) p += __shfl_xor(p, d, 64);
+            if ((t & 31) == 0) {
+                const int bk = q >> 5;
+                co[bk] = p & 0xffffu;
+                // the last bucket also holds the value 2^15
+                co[128 + bk] = (p >> 16) + (bk == 127 ? (h[kQTop / 2] + h[kQStride + kQTop / 2]) & 0xffffu : 0u);
+            }
+        }
+        if (t == 0) {  // the group of the value 2^15 and the padding words
+            const uint4 x = h4[kQTop / 8], y = g4[kQTop / 8];
+            out[kQTop / 8] = make_uint4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+        }
+        __syncthreads();  // the next row clears the counts this row has read
     }
 }
 
@@ -232,11 +256,9 @@ __global__ __launch_bounds__(kQThreads) void qhist_kernel(const int64_t *offsets
 // bucket, the bucket holding the exact rank j, then the counts of its values
 // summed over the parts, and the value where the cumulative count reaches j.
 // Every thread issues its share of the B rows' loads together.
-__global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offsets,
-                                                            const int32_t *seg, const float *c_p,
-                                                            const float *c_w, const uint32_t *fine,
-                                                            const uint32_t *coarse, int B,
-                                                            int32_t *q_value, int64_t *q_rank)
+__device__ void qselect_class(const int64_t *offsets, const int32_t *seg, const float *c_p,
+                              const float *c_w, const uint32_t *fine, const uint32_t *coarse, int B0,
+                              const int64_t *boff, int c, int32_t *q_value, int64_t *q_rank)
 {
     constexpr int kG = kQThreads / kQBuckets;  // row groups of the coarse sum
     constexpr int kF = 129;                    // values of a bucket (the last adds 2^15)
@@ -248,15 +270,18 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
     __shared__ long long sel_below;
     __shared__ int64_t s_off[2], s_rank;
     __shared__ float s_cost[2];
-    const int c = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int s = seg_of_x(seg, c);
     // the rank's inputs, loaded by every thread from addresses that differ by
     // lane: vector loads in flight with the coarse loads below, not waited for
     // before them as uniform scalar loads would be
     const int64_t r_off = offsets[s + (t & 1)];
     const float r_cost = ((t & 2) ? c_w : c_p)[c];
-    const uint32_t *cs = coarse + (long long)s * B * kQBuckets;
-    const uint32_t *fs = fine + (long long)s * B * kQStride;
+    // the segment's rows: B0 per segment, or those of the table boff
+    const long long row0 = boff ? boff[s] : (long long)s * B0;
+    const int B = boff ? (int)(boff[s + 1] - row0) : B0;
+    const uint32_t *cs = coarse + row0 * kQBuckets;
+    const uint32_t *fs = fine + row0 * kQStride;
     {
         const int q = t % kQBuckets, g = t / kQBuckets;
         uint32_t a = 0;
@@ -349,6 +374,20 @@ __global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offse
     if (t == 0) q_rank[c] = j;
 }
 
+// classes in a block-uniform loop; the barrier lets the next class reuse the LDS
+__global__ __launch_bounds__(kQThreads) void qselect_kernel(const int64_t *offsets,
+                                                            const int32_t *seg, const float *c_p,
+                                                            const float *c_w, const uint32_t *fine,
+                                                            const uint32_t *coarse, int B,
+                                                            const int64_t *boff, int C,
+                                                            int32_t *q_value, int64_t *q_rank)
+{
+    for (int c = blockIdx.x; c < C; c += gridDim.x) {
+        qselect_class(offsets, seg, c_p, c_w, fine, coarse, B, boff, c, q_value, q_rank);
+        __syncthreads();
+    }
+}
+
 hipError_t select_prepare();
 hipError_t qhist_prepare();
 
@@ -399,14 +438,12 @@ __device__ int64_t exact_rank(float cp, float cw, int64_t N)
 // smallest sample is the first value whose cumulative count reaches j.
 constexpr int kSelThreads = 1024;
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offsets,
-                                                             const int32_t *seg, const float *c_p,
-                                                             const float *c_w, const uint32_t *hist,
-                                                             int32_t *q_value, int64_t *q_rank)
+__device__ void select_class(const int64_t *offsets, const int32_t *seg, const float *c_p,
+                             const float *c_w, const uint32_t *hist, int c, uint32_t *hl,
+                             int32_t *q_value, int64_t *q_rank)
 {
-    extern __shared__ uint32_t hl[];  // the segment's histogram, kHistBins words
     __shared__ uint64_t sc[kSelThreads / 64];
-    const int c = blockIdx.x, t = threadIdx.x;
+    const int t = threadIdx.x;
     const int s = seg_of_x(seg, c);
     const int64_t N = offsets[s + 1] - offsets[s];
     const uint32_t *h = hist + (long long)s * kHistBins;
@@ -459,6 +496,19 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offs
     if (t == 0) q_rank[c] = j;
 }
 
+// classes in a block-uniform loop; the barrier lets the next class reuse the LDS
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const int64_t *offsets,
+                                                             const int32_t *seg, const float *c_p,
+                                                             const float *c_w, const uint32_t *hist,
+                                                             int C, int32_t *q_value, int64_t *q_rank)
+{
+    extern __shared__ uint32_t hl[];  // the segment's histogram, kHistBins words
+    for (int c = blockIdx.x; c < C; c += gridDim.x) {
+        select_class(offsets, seg, c_p, c_w, hist, c, hl, q_value, q_rank);
+        __syncthreads();
+    }
+}
+
 hipError_t select_prepare()
 {
     return hipFuncSetAttribute(reinterpret_cast<const void *>(select_kernel),
@@ -470,8 +520,9 @@ hipError_t launch_select(const int64_t *offsets, const int32_t *seg, const float
                          const float *c_w, const uint32_t *hist, int C, int32_t *q_value,
                          int64_t *q_rank, hipStream_t st)
 {
-    hipLaunchKernelGGL(select_kernel, dim3(C), dim3(kSelThreads), kHistBins * sizeof(uint32_t), st,
-                       offsets, seg, c_p, c_w, hist, q_value, q_rank);
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)std::min((long long)C, kMaxGridBlocks)),
+                       dim3(kSelThreads), kHistBins * sizeof(uint32_t), st, offsets, seg, c_p, c_w,
+                       hist, C, q_value, q_rank);
     return hipGetLastError();
 }
 
@@ -482,22 +533,25 @@ hipError_t qhist_prepare()
                                (int)(2 * kQStride * sizeof(uint32_t)));
 }
 
-int qhist_parts(int S, long long max_seg, int num_cu)
+long long qhist_parts(int S, long long n, int num_cu)
 {
-    const long long need = (max_seg + kQMaxPart - 1) / kQMaxPart;
-    return (int)std::max((long long)hist_parts(S, max_seg, num_cu), std::max(1LL, need));
+    const long long need = (n + kQMaxPart - 1) / kQMaxPart;
+    return std::max((long long)hist_parts(S, n, num_cu), std::max(1LL, need));
 }
 
 hipError_t launch_class_quantile(const int64_t *offsets, const int32_t *seg, const int32_t *xi,
                                  const float *c_p, const float *c_w, int S, int C, int B,
-                                 uint32_t *fine, uint32_t *coarse, int32_t *q_value,
-                                 int64_t *q_rank, hipStream_t st)
+                                 const int64_t *boff, long long rows, uint32_t *fine,
+                                 uint32_t *coarse, int32_t *q_value, int64_t *q_rank,
+                                 hipStream_t st)
 {
-    hipLaunchKernelGGL(qhist_kernel, dim3((unsigned)((long long)S * B)), dim3(kQThreads),
-                       2 * kQStride * sizeof(uint32_t), st, offsets, xi, B, fine, coarse);
+    hipLaunchKernelGGL(qhist_kernel, dim3((unsigned)std::min(rows, kMaxGridBlocks)), dim3(kQThreads),
+                       2 * kQStride * sizeof(uint32_t), st, offsets, xi, S, B, boff, rows, fine,
+                       coarse);
     HIPRET(hipGetLastError());
-    hipLaunchKernelGGL(qselect_kernel, dim3((unsigned)C), dim3(kQThreads), 0, st, offsets, seg, c_p,
-                       c_w, fine, coarse, B, q_value, q_rank);
+    hipLaunchKernelGGL(qselect_kernel, dim3((unsigned)std::min((long long)C, kMaxGridBlocks)),
+                       dim3(kQThreads), 0, st, offsets, seg, c_p, c_w, fine, coarse, B, boff, C,
+                       q_value, q_rank);
     return hipGetLastError();
 }
 
@@ -925,12 +979,11 @@ __global__ __launch_bounds__(64 * kTableWaves) void exact_table_kernel(
 
 // Block per (e, c): lowest k <= kmax with the smallest W, and the values there
 // (the exact optimum over a W table whose entries are exact-spec values).
-__global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, const int32_t *m_star,
-                                                           const int32_t *k_max, int C, int K,
-                                                           int32_t *k_star, double *W_star,
-                                                           int32_t *m_at_star)
+__device__ void table_argmin_row(const double *W, const int32_t *m_star, const int32_t *k_max,
+                                int C, int K, int ec, int32_t *k_star, double *W_star,
+                                int32_t *m_at_star)
 {
-    const int ec = blockIdx.x, c = ec % C, t = threadIdx.x;
+    const int c = ec % C, t = threadIdx.x;
     int kmax = K - 1;
     if (k_max) {
         kmax = k_max[c];
@@ -967,12 +1020,25 @@ __global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, cons
     }
 }
 
+// rows (e, c) in a block-uniform loop; the barrier lets the next row reuse the LDS
+__global__ __launch_bounds__(256) void table_argmin_kernel(const double *W, const int32_t *m_star,
+                                                           const int32_t *k_max, int C, int K,
+                                                           int rows, int32_t *k_star, double *W_star,
+                                                           int32_t *m_at_star)
+{
+    for (int ec = blockIdx.x; ec < rows; ec += gridDim.x) {
+        table_argmin_row(W, m_star, k_max, C, K, ec, k_star, W_star, m_at_star);
+        __syncthreads();
+    }
+}
+
 hipError_t launch_table_argmin(const double *W, const int32_t *m_star, const int32_t *k_max,
                                int E, int C, int K, int32_t *k_star, double *W_star,
                                int32_t *m_at_star, hipStream_t st)
 {
-    hipLaunchKernelGGL(table_argmin_kernel, dim3((unsigned)((long long)E * C)), dim3(256), 0, st, W,
-                       m_star, k_max, C, K, k_star, W_star, m_at_star);
+    const long long rows = (long long)E * C;  // below 2^31: checked by the entry points
+    hipLaunchKernelGGL(table_argmin_kernel, dim3((unsigned)std::min(rows, kMaxGridBlocks)), dim3(256),
+                       0, st, W, m_star, k_max, C, K, (int)rows, k_star, W_star, m_at_star);
     return hipGetLastError();
 }
 
@@ -985,8 +1051,7 @@ hipError_t launch_exact_table(const int64_t *offsets, const int32_t *seg, const 
 {
     HIPRET(launch_prefix(hist, S, cnt, sum, st));
     const long long rows = (long long)C * K;
-    // at most 2^20 blocks: the grid's work-item count stays below 2^32
-    const long long blocks = std::min((rows + kTableWaves - 1) / kTableWaves, 1LL << 20);
+    const long long blocks = std::min((rows + kTableWaves - 1) / kTableWaves, kMaxGridBlocks);
     hipLaunchKernelGGL(exact_table_kernel, dim3((unsigned)blocks),
                        dim3(64 * kTableWaves), 0, st, offsets, seg, L, eta, lam, c_p, c_w, eps,
                        (const uint32_t *)cnt, (const uint64_t *)sum, E, C, K, M, W, m_star);
@@ -1119,38 +1184,39 @@ __global__ __launch_bounds__(256) void continuous_dual_kernel(
     const float *c_p, const float *c_w, const float *eps, const uint32_t *cnt, const uint64_t *sum,
     int E, int C, int K, double *W, double *gamma)
 {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (long long)E * C * K) return;
-    const int k = (int)(i % K);
-    const int ec = (int)(i / K), c = ec % C, e = ec / C;
-    const int s = seg_of_x(seg, c);
-    SegStats st;
-    st.cnt = cnt + (long long)s * kHistBins;
-    st.sum = sum + (long long)s * kHistBins;
-    st.N = (double)(offsets[s + 1] - offsets[s]);
-    st.SX = (double)st.sum[kHistBins - 1];
-    const int Li = L_[c];
-    st.tmax = Li < kHistBins - 1 ? Li : kHistBins - 1;
-    const double L = (double)Li, eta = (double)eta_[k];
-    const double cw = (double)c_w[c], cp = (double)c_p[c];
-    const double B = cw * eta, Cc = cp * (L - eta);
-    const double ev = (double)eps[(long long)e * C + c];
-    double J, dJ;
-    double lo = 0.0, hi = cw > cp ? cw : cp;
-    dual_at(st, B, Cc, L, cw, cp, ev, 0.0, J, dJ);
-    if (!(dJ >= 0.0)) {
-        for (int it = 0; it < 200 && hi - lo > 0.0; ++it) {
-            const double mid = 0.5 * (lo + hi);
-            if (mid <= lo || mid >= hi) break;
-            dual_at(st, B, Cc, L, cw, cp, ev, mid, J, dJ);
-            if (dJ >= 0.0) hi = mid;
-            else lo = mid;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < (long long)E * C * K;
+         i += (long long)gridDim.x * blockDim.x) {
+        const int k = (int)(i % K);
+        const int ec = (int)(i / K), c = ec % C, e = ec / C;
+        const int s = seg_of_x(seg, c);
+        SegStats st;
+        st.cnt = cnt + (long long)s * kHistBins;
+        st.sum = sum + (long long)s * kHistBins;
+        st.N = (double)(offsets[s + 1] - offsets[s]);
+        st.SX = (double)st.sum[kHistBins - 1];
+        const int Li = L_[c];
+        st.tmax = Li < kHistBins - 1 ? Li : kHistBins - 1;
+        const double L = (double)Li, eta = (double)eta_[k];
+        const double cw = (double)c_w[c], cp = (double)c_p[c];
+        const double B = cw * eta, Cc = cp * (L - eta);
+        const double ev = (double)eps[(long long)e * C + c];
+        double J, dJ;
+        double lo = 0.0, hi = cw > cp ? cw : cp;
+        dual_at(st, B, Cc, L, cw, cp, ev, 0.0, J, dJ);
+        if (!(dJ >= 0.0)) {
+            for (int it = 0; it < 200 && hi - lo > 0.0; ++it) {
+                const double mid = 0.5 * (lo + hi);
+                if (mid <= lo || mid >= hi) break;
+                dual_at(st, B, Cc, L, cw, cp, ev, mid, J, dJ);
+                if (dJ >= 0.0) hi = mid;
+                else lo = mid;
+            }
+            dual_at(st, B, Cc, L, cw, cp, ev, hi, J, dJ);
+            lo = hi;
         }
-        dual_at(st, B, Cc, L, cw, cp, ev, hi, J, dJ);
-        lo = hi;
+        W[i] = J;
+        gamma[i] = lo;
     }
-    W[i] = J;
-    gamma[i] = lo;
 }
 
 hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, const int32_t *L,
@@ -1161,7 +1227,8 @@ hipError_t launch_continuous_dual(const int64_t *offsets, const int32_t *seg, co
 {
     HIPRET(launch_prefix(hist, S, cnt, sum, st));
     const long long n = (long long)E * C * K;
-    hipLaunchKernelGGL(continuous_dual_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+    hipLaunchKernelGGL(continuous_dual_kernel, dim3((unsigned)std::min((n + 255) / 256, kMaxGridBlocks)),
+                       dim3(256), 0, st,
                        offsets, seg, L, eta, c_p, c_w, eps, (const uint32_t *)cnt,
                        (const uint64_t *)sum, E, C, K, W, gamma);
     return hipGetLastError();

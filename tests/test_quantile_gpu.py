@@ -1,8 +1,10 @@
 """class_quantile against the oracle's order statistic, on the cases that stress
 its layout: 16-bit counts packed two to a word (values below and above 2^14),
 the value 2^15 itself, ranks on the first and last value of a coarse bucket,
-segments long enough to need more blocks than the default, classes aliasing
-one segment, constant samples, and cost ratios that put the rank at 1 or N
+segments long enough to need more blocks than the default, segments with
+unequal block counts (many short segments beside one long one, read through
+a row table), classes aliasing one segment, constant samples, and cost ratios
+that put the rank at 1 or N
 (Prop. 4.2: the critical fractile c_p / (c_p + c_w), read as the
 generalised-inverse order statistic).  Bar: q_value and q_rank bit for bit.
 """
@@ -133,3 +135,27 @@ def test_repeated_calls_and_shrinking_problem(ctx, dev):
                                 .astype(np.int32) for _ in range(2)], [2.0, 60.0], [1.0, 1.0])
     for w in (big, small, big, small):
         _check(ctx, dev, w)
+
+
+@pytest.mark.parametrize("n_small,n_big", [(300, 3_000_001), (2000, 1 << 24)])
+def test_segments_with_unequal_part_counts(ctx, dev, n_small, n_big):
+    # one long segment among many short ones: the long one is split into
+    # ceil(n / 65535) blocks, every short one takes one, and the rows of a
+    # segment are found through the row table (with one count of blocks for
+    # all segments, 2000 + 1 segments of up to 2^24 samples would need 514k rows)
+    rng = np.random.default_rng(16 + n_small)
+    parts = [rng.integers(1, 32769, int(rng.integers(1, 201))).astype(np.int32)
+             for _ in range(n_small)]
+    big = np.clip(np.rint(rng.lognormal(6.0, 1.4, n_big)), 1, 32768).astype(np.int32)
+    big[::9973] = 32768
+    mid = n_small // 2
+    parts.insert(mid, big)
+    S = len(parts)
+    C = S + 99
+    seg = [c % S for c in range(C)]
+    seg[1] = seg[S] = seg[S + 7] = mid  # three more classes on the long segment
+    r = rng.uniform(-17, 17, C)
+    c_p = _f32(np.where(r >= 0, 2.0 ** 7, 2.0 ** (7 + r)))
+    c_w = _f32(np.where(r >= 0, 2.0 ** (7 - r), 2.0 ** 7))
+    w = _workload(f"unequal-{n_small}", parts, c_p, c_w, seg=seg)
+    _check(ctx, dev, w)
