@@ -86,6 +86,7 @@ RANDOM_CASES = [
     dict(seed=13, C=2, N=(500, 60), L=700, K=50, M=2, E=3),                 # 2 multipliers
     dict(seed=14, C=3, N=(400, 90, 1200), L=900, K=21, M=300, E=70),       # 70 radii, 300 multipliers
     dict(seed=15, C=2, N=(300, 50), L=500, K=17, M=9, E=1000),              # 1000 radii: 16 lane-group passes
+    dict(seed=16, C=2, N=(40, 3), L=0, K=1, M=5, E=2, dist="constant"),  # L = 0: every sample and level 0
 ]
 
 
