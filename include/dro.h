@@ -36,6 +36,11 @@
  *    grid order, coefficient range) is checked by dro_validate; kernels never
  *    read outside the segments given by the offsets, whatever the data.
  *  - A ctx is not thread-safe: use one ctx per host thread / stream.
+ *  - HIP graphs: once a call has run with the same problem on the same stream
+ *    (sizing the workspace and staging the offsets), class_quantile,
+ *    dro_cost_eval and dro_argmin_reservation enqueue kernels only, with no
+ *    allocation, host copy or memset, so a stream capture of them replays
+ *    correctly.
  *  - Exactness limits (DRO_ELIMIT when exceeded): 0 <= x, eta <= L <= 2^15,
  *    N_c <= 2^26 samples per class, every lam, c_p, c_w in [2^-10, 2^7];
  *    K <= 2^15 + 1 grid points, M <= 65536 multipliers, K * M < 2^31 pairs,
