@@ -164,17 +164,19 @@ __device__ int64_t exact_rank(float cp, float cw, int64_t N);
 // ---- class_quantile: per-block histograms, then one select per class ----
 //
 // Block for row r (segment s, part b of its B_s parts, at most kQMaxPart
-// samples; rows in a block-uniform loop) counts its share
-// in LDS with 16-bit counts packed two to a word (value v < 2^15 in word
-// v mod 2^14, low half for v < 2^14, high half above; 2^15 in the low half of
-// word 2^14), in two copies: even threads add into one, odd threads into the
-// other, which halves the lanes of one wave that meet on one LDS word when
-// short lengths repeat.  It then stores, with plain 16-byte stores, the two
-// copies' sum (every count fits 16 bits, as the block holds at most 65,535
-// samples) and, in the same pass, its counts per coarse bucket of 128 values.
-// No global atomics: the select reads the B rows of the bucket it needs.  The
-// rows are written with non-temporal stores, as only the select reads them,
-// once (on mixture-16x1M 1.4 us less per launch than plain stores).
+// samples; rows in a block-uniform loop) counts its share in LDS with 16-bit
+// counts packed two to a word (value v < 2^15 in word v mod 2^14, low half
+// for v < 2^14, high half above; 2^15 in the low half of word 2^14), in two
+// copies: even threads add into one, odd threads into the other, which halves
+// the lanes of one wave that meet on one LDS word when short lengths repeat.
+// It then stores the two copies' sum (every count fits 16 bits, as the block
+// holds at most 65,535 samples) with 16-byte non-temporal stores, as only the
+// select reads it, once (on mixture-16x1M 1.4 us less per launch than plain
+// stores), and, in the same pass, its counts per coarse bucket of 128 values.
+// Segment s owns rows s B .. s B + B - 1 when every segment has B parts, else
+// rows boff[s] .. boff[s + 1] - 1 of a table built by the host, in which the
+// block finds its segment by bisection.  No global atomics: the select reads
+// the segment's rows of the bucket it needs.
 constexpr int kQThreads = 1024;
 typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
 
@@ -252,10 +254,11 @@ __global__ __launch_bounds__(kQThreads) void qhist_kernel(const int64_t *offsets
     }
 }
 
-// Block per class c (segment s): the coarse counts of the B parts summed per
-// bucket, the bucket holding the exact rank j, then the counts of its values
-// summed over the parts, and the value where the cumulative count reaches j.
-// Every thread issues its share of the B rows' loads together.
+// Class c (segment s, its B rows at s B0 or boff[s]; classes in a
+// block-uniform loop): the coarse counts of the rows summed per bucket, the
+// bucket holding the exact rank j, then the counts of its values summed over
+// the rows, and the value where the cumulative count reaches j.  Every thread
+// issues its share of the rows' loads together.
 __device__ void qselect_class(const int64_t *offsets, const int32_t *seg, const float *c_p,
                               const float *c_w, const uint32_t *fine, const uint32_t *coarse, int B0,
                               const int64_t *boff, int c, int32_t *q_value, int64_t *q_rank)
